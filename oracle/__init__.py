@@ -1,0 +1,273 @@
+"""CPU oracle for the tuned-GEMM path — TEST INFRASTRUCTURE ONLY.
+
+Only the tests, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` may import this package. It wraps ``oracle.c`` (plain C, fp64,
+built with gcc) through ctypes and shares no code with the GPU library:
+
+* ``gemm`` / ``gemm_entries`` — C = A·B by the three-loop definition (§3.2),
+  fp64, on the exact widening of the input bytes.
+* ``Space`` — the configuration space of Eq.1–4, rank/unrank in the frozen
+  canonical order, legitimacy J (Eq.5), neighbours g(s) (Eq.6, Eq.9).
+* ``gbfs`` — Alg.1 (§4.2) with a caller-supplied cost function.
+
+Parity unpinned: the hardware part of J (register, LDS and grid limits) has
+no value in the paper to pin it; it is checked by hand-worked cases and by
+every J=1 configuration launching on the GPU.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+F32, BF16 = 0, 1
+ADJACENT, ANY_PAIR = 0, 1
+MAXD = 4
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c with gcc into liboracle.so (beside the source)."""
+    if force or not os.path.exists(_LIB):
+        cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-shared", "-fPIC",
+               _SRC, "-o", _LIB + ".tmp", "-lpthread", "-lm"]
+        subprocess.run(cmd, check=True)
+        os.replace(_LIB + ".tmp", _LIB)
+    return _LIB
+
+
+class _Space(ctypes.Structure):
+    _fields_ = [("M", ctypes.c_int64), ("N", ctypes.c_int64), ("K", ctypes.c_int64),
+                ("d", ctypes.c_int32 * 3), ("dtype", ctypes.c_int32),
+                ("mfma_coord", ctypes.c_int32), ("mode", ctypes.c_int32)]
+
+
+class _Config(ctypes.Structure):
+    _fields_ = [("f", (ctypes.c_int64 * MAXD) * 3), ("mfma", ctypes.c_int32),
+                ("legit", ctypes.c_int32)]
+
+
+class _GbfsResult(ctypes.Structure):
+    _fields_ = [("best", _Config), ("best_cost", ctypes.c_double),
+                ("timed", ctypes.c_int64), ("popped", ctypes.c_int64)]
+
+
+_COST_FN = ctypes.CFUNCTYPE(ctypes.c_double, ctypes.POINTER(_Config), ctypes.c_uint64,
+                            ctypes.c_void_p)
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=False)
+        L = ctypes.CDLL(_LIB)
+        p, i64, u64 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64
+        L.oracle_gemm.argtypes = [i64, i64, i64, p, p, ctypes.c_int, p, ctypes.c_int]
+        L.oracle_gemm_entries.argtypes = [i64, i64, i64, p, p, ctypes.c_int, i64, p, p, p]
+        L.oracle_widen.argtypes = [p, ctypes.c_int, i64, p]
+        L.or_dim_tuples.argtypes = [i64, ctypes.c_int, p, i64]
+        L.or_dim_tuples.restype = i64
+        SP, CF = ctypes.POINTER(_Space), ctypes.POINTER(_Config)
+        L.or_space_size.argtypes = [SP, ctypes.POINTER(u64)]
+        L.or_rank.argtypes = [SP, CF, ctypes.POINTER(u64)]
+        L.or_unrank.argtypes = [SP, u64, CF]
+        L.or_member.argtypes = [SP, CF]
+        L.or_legit.argtypes = [SP, CF]
+        L.or_enumerate.argtypes = [SP, u64, u64, CF]
+        L.or_neighbours.argtypes = [SP, CF, CF, ctypes.c_int]
+        L.or_splitmix64_next.argtypes = [ctypes.POINTER(u64)]
+        L.or_splitmix64_next.restype = u64
+        L.or_gbfs.argtypes = [SP, CF, ctypes.c_int, i64, u64, _COST_FN, p,
+                              ctypes.POINTER(_GbfsResult), p, p, i64]
+        _lib = L
+    return _lib
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _dtype_code(dtype) -> int:
+    return {"f32": F32, "bf16": BF16, F32: F32, BF16: BF16}[dtype]
+
+
+# ---------------------------------------------------------------------------
+# GEMM
+# ---------------------------------------------------------------------------
+
+def gemm(A_bytes: np.ndarray, B_bytes: np.ndarray, M: int, N: int, K: int, dtype,
+         nthreads: int | None = None) -> np.ndarray:
+    """fp64 C (M×N) from the raw row-major input bytes (see workloads.raw_bytes)."""
+    dt = _dtype_code(dtype)
+    esz = 4 if dt == F32 else 2
+    A_bytes = np.ascontiguousarray(A_bytes, dtype=np.uint8)
+    B_bytes = np.ascontiguousarray(B_bytes, dtype=np.uint8)
+    assert A_bytes.size == M * K * esz and B_bytes.size == K * N * esz
+    C = np.empty((M, N), dtype=np.float64)
+    nt = nthreads or os.cpu_count() or 1
+    rc = lib().oracle_gemm(M, N, K, _ptr(A_bytes), _ptr(B_bytes), dt, _ptr(C), nt)
+    if rc:
+        raise MemoryError("oracle_gemm failed")
+    return C
+
+
+def gemm_entries(A_bytes, B_bytes, M, N, K, dtype, rows, cols) -> np.ndarray:
+    dt = _dtype_code(dtype)
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    cols = np.ascontiguousarray(cols, dtype=np.int64)
+    out = np.empty(rows.size, dtype=np.float64)
+    A_bytes = np.ascontiguousarray(A_bytes, dtype=np.uint8)
+    B_bytes = np.ascontiguousarray(B_bytes, dtype=np.uint8)
+    rc = lib().oracle_gemm_entries(M, N, K, _ptr(A_bytes), _ptr(B_bytes), dt, rows.size,
+                                   _ptr(rows), _ptr(cols), _ptr(out))
+    if rc:
+        raise IndexError("entry out of range")
+    return out
+
+
+def widen(raw: np.ndarray, dtype) -> np.ndarray:
+    dt = _dtype_code(dtype)
+    raw = np.ascontiguousarray(raw, dtype=np.uint8)
+    n = raw.size // (4 if dt == F32 else 2)
+    out = np.empty(n, dtype=np.float64)
+    lib().oracle_widen(_ptr(raw), dt, n, _ptr(out))
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Configuration space
+# ---------------------------------------------------------------------------
+
+def dim_tuples(D: int, d: int) -> list:
+    L = lib()
+    n = L.or_dim_tuples(D, d, None, 0)
+    buf = np.zeros(max(n * d, 1), dtype=np.int64)
+    L.or_dim_tuples(D, d, _ptr(buf), n)
+    return [tuple(int(v) for v in buf[i * d:(i + 1) * d]) for i in range(n)]
+
+
+class Space:
+    """A configuration space; configs are tuples (m_levels, k_levels, n_levels, mfma)."""
+
+    def __init__(self, M, N, K, d=(4, 4, 4), dtype="f32", mfma_coord=False,
+                 mode=ADJACENT):
+        self.M, self.N, self.K = int(M), int(N), int(K)
+        self.d = tuple(int(x) for x in d)
+        self.dtype = _dtype_code(dtype)
+        self.mfma_coord = bool(mfma_coord)
+        self.mode = int(mode)
+        s = _Space()
+        s.M, s.N, s.K = self.M, self.N, self.K
+        for i in range(3):
+            s.d[i] = self.d[i]
+        s.dtype, s.mfma_coord, s.mode = self.dtype, int(self.mfma_coord), self.mode
+        self._s = s
+
+    # -- conversions --
+    def _to_c(self, cfg) -> _Config:
+        c = _Config()
+        for x in range(3):
+            lv = cfg[x]
+            assert len(lv) == self.d[x], (cfg, self.d)
+            for i, v in enumerate(lv):
+                c.f[x][i] = int(v)
+        c.mfma = int(cfg[3]) if len(cfg) > 3 else 0
+        return c
+
+    def _from_c(self, c: _Config):
+        return (tuple(int(c.f[0][i]) for i in range(self.d[0])),
+                tuple(int(c.f[1][i]) for i in range(self.d[1])),
+                tuple(int(c.f[2][i]) for i in range(self.d[2])),
+                int(c.mfma))
+
+    # -- queries --
+    def size(self) -> int:
+        out = ctypes.c_uint64()
+        assert lib().or_space_size(ctypes.byref(self._s), ctypes.byref(out)) == 0
+        return int(out.value)
+
+    def rank(self, cfg) -> int:
+        out = ctypes.c_uint64()
+        rc = lib().or_rank(ctypes.byref(self._s), ctypes.byref(self._to_c(cfg)),
+                           ctypes.byref(out))
+        if rc:
+            raise ValueError(f"not a member: {cfg}")
+        return int(out.value)
+
+    def unrank(self, r: int):
+        c = _Config()
+        if lib().or_unrank(ctypes.byref(self._s), int(r), ctypes.byref(c)):
+            raise IndexError(r)
+        return self._from_c(c)
+
+    def member(self, cfg) -> bool:
+        return bool(lib().or_member(ctypes.byref(self._s), ctypes.byref(self._to_c(cfg))))
+
+    def legit(self, cfg) -> bool:
+        return bool(lib().or_legit(ctypes.byref(self._s), ctypes.byref(self._to_c(cfg))))
+
+    def enumerate(self, start: int = 0, count: int | None = None):
+        """List of (cfg, J) for ranks [start, start+count)."""
+        if count is None:
+            count = self.size() - start
+        arr = (_Config * max(count, 1))()
+        rc = lib().or_enumerate(ctypes.byref(self._s), start, count, arr)
+        assert rc == 0
+        return [(self._from_c(arr[i]), bool(arr[i].legit)) for i in range(count)]
+
+    def enumerate_raw(self, start: int, count: int) -> np.ndarray:
+        """Raw config records as a numpy structured view (for bulk comparisons)."""
+        arr = (_Config * max(count, 1))()
+        assert lib().or_enumerate(ctypes.byref(self._s), start, count, arr) == 0
+        return np.frombuffer(arr, dtype=np.uint8).reshape(max(count, 1), ctypes.sizeof(_Config))[:count]
+
+    def neighbours(self, cfg):
+        """g(s) in ascending rank: list of (cfg, J)."""
+        out = (_Config * (3 * MAXD * MAXD + 1))()
+        n = lib().or_neighbours(ctypes.byref(self._s), ctypes.byref(self._to_c(cfg)), out,
+                                3 * MAXD * MAXD + 1)
+        if n < 0:
+            raise ValueError(f"not a member: {cfg}")
+        return [(self._from_c(out[i]), bool(out[i].legit)) for i in range(n)]
+
+    def paper_s0(self):
+        """The paper's start state: [D,1,…,1] per dimension (§5), MFMA 16."""
+        return (tuple([self.M] + [1] * (self.d[0] - 1)),
+                tuple([self.K] + [1] * (self.d[1] - 1)),
+                tuple([self.N] + [1] * (self.d[2] - 1)),
+                16 if self.mfma_coord else 0)
+
+
+def splitmix64_stream(seed: int, n: int) -> list:
+    st = ctypes.c_uint64(seed)
+    return [int(lib().or_splitmix64_next(ctypes.byref(st))) for _ in range(n)]
+
+
+def gbfs(space: Space, s0, rho: int, budget: int, seed: int, cost_fn):
+    """Run Alg.1. ``cost_fn(cfg, rank) -> float``. Returns a dict with the best
+    configuration, its cost, the count timed, the pops, and the timing log."""
+    log_r = np.zeros(budget, dtype=np.uint64)
+    log_c = np.zeros(budget, dtype=np.float64)
+
+    def _cb(cptr, rank, _ctx):
+        return float(cost_fn(space._from_c(cptr.contents), int(rank)))
+
+    cb = _COST_FN(_cb)
+    res = _GbfsResult()
+    rc = lib().or_gbfs(ctypes.byref(space._s), ctypes.byref(space._to_c(s0)), int(rho),
+                       int(budget), int(seed), cb, None, ctypes.byref(res), _ptr(log_r),
+                       _ptr(log_c), budget)
+    if rc:
+        raise ValueError("or_gbfs: bad argument (illegitimate s0, budget < 1 or rho < 1)")
+    n = int(res.timed)
+    return {"best": space._from_c(res.best), "best_cost": float(res.best_cost),
+            "timed": n, "popped": int(res.popped),
+            "log_ranks": [int(v) for v in log_r[:n]], "log_costs": [float(v) for v in log_c[:n]]}

@@ -1,0 +1,92 @@
+/*
+ * oracle.h — plain CPU reference for the tuned-GEMM path.
+ *
+ * TEST INFRASTRUCTURE ONLY. Only the tests, the smoke check and the
+ * benchmark's CPU-baseline leg may load this library. It shares no code,
+ * header or helper with the GPU library; everything here is written from the
+ * paper and from the frozen definitions of the configuration space.
+ *
+ *   - oracle_gemm*: C = A·B in fp64 by the plain three-loop definition (§3.2),
+ *     on the exact fp64 widening of the fp32 or bf16 input bytes.
+ *   - or_*: the configuration space of Eq.1–4 (power-of-two factors, odd
+ *     cofactor at level 0), the state legitimacy bit J of Eq.5, the action set
+ *     of Eq.6 / neighbour list of Eq.9, and the G-BFS of Alg.1 (§4.2).
+ *
+ * Parity pins: see tests/test_oracle_*.py. The legitimacy predicate beyond
+ * membership (the hardware constraints) has no paper pin: "parity unpinned"
+ * as to its hardware meaning; it is pinned only by hand-worked cases and by
+ * every J=1 configuration launching on the GPU.
+ */
+#ifndef GEMM_ORACLE_H
+#define GEMM_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { OR_F32 = 0, OR_BF16 = 1 };
+enum { OR_ADJACENT = 0, OR_ANY_PAIR = 1 };
+#define OR_MAXD 4
+
+typedef struct {
+  int64_t M, N, K;
+  int32_t d[3];        /* levels per dimension, order m, k, n */
+  int32_t dtype;       /* OR_F32 / OR_BF16 */
+  int32_t mfma_coord;  /* 1: MFMA size {16,32} is a coordinate */
+  int32_t mode;        /* OR_ADJACENT / OR_ANY_PAIR */
+} or_space;
+
+typedef struct {
+  int64_t f[3][OR_MAXD]; /* f[0]: m levels, f[1]: k levels, f[2]: n levels */
+  int32_t mfma;          /* 16/32 with the coordinate, 0 without */
+  int32_t legit;         /* J, filled by the functions that return configs */
+} or_config;
+
+/* fp64 GEMM, C (M×N, row-major doubles) = A (M×K) · B (K×N), row-major input
+ * bytes of the given dtype. Threads over row blocks. Returns 0. */
+int oracle_gemm(int64_t M, int64_t N, int64_t K, const void* A, const void* B,
+                int dtype, double* C, int nthreads);
+/* C*[rows[t]][cols[t]] for t < n (sampled entries at any size). */
+int oracle_gemm_entries(int64_t M, int64_t N, int64_t K, const void* A,
+                        const void* B, int dtype, int64_t n,
+                        const int64_t* rows, const int64_t* cols, double* out);
+/* Exact widening of input bytes to fp64 (n elements). */
+int oracle_widen(const void* src, int dtype, int64_t n, double* dst);
+
+/* Tuples of one dimension in canonical (lexicographic) order; returns the
+ * count, writes count*d values when out != NULL and count <= cap. */
+int64_t or_dim_tuples(int64_t D, int d, int64_t* out, int64_t cap);
+int or_space_size(const or_space* sp, uint64_t* size);
+int or_rank(const or_space* sp, const or_config* c, uint64_t* rank);
+int or_unrank(const or_space* sp, uint64_t rank, or_config* c);
+int or_member(const or_space* sp, const or_config* c);
+int or_legit(const or_space* sp, const or_config* c);
+/* Configurations with ranks [start, start+count) written to out. */
+int or_enumerate(const or_space* sp, uint64_t start, uint64_t count,
+                 or_config* out);
+/* Neighbour list g(s) (Eq.9) in ascending rank; returns the count or -1 if
+ * cap is too small. Each entry carries its J. */
+int or_neighbours(const or_space* sp, const or_config* s, or_config* out,
+                  int cap);
+
+uint64_t or_splitmix64_next(uint64_t* state);
+
+typedef double (*or_cost_fn)(const or_config* c, uint64_t rank, void* ctx);
+typedef struct {
+  or_config best;
+  double best_cost;
+  int64_t timed;
+  int64_t popped;
+} or_gbfs_result;
+/* G-BFS, Alg.1. log_ranks/log_costs (cap log_cap) receive every timed
+ * configuration in timing order. Returns 0, or -1 on a bad argument
+ * (s0 illegitimate, budget < 1, rho < 1). */
+int or_gbfs(const or_space* sp, const or_config* s0, int rho, int64_t budget,
+            uint64_t seed, or_cost_fn cost, void* ctx, or_gbfs_result* res,
+            uint64_t* log_ranks, double* log_costs, int64_t log_cap);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
