@@ -348,7 +348,7 @@ int or_legit(const or_space* sp, const or_config* c) {
   const int64_t BM = wM * rM * bM, BN = wN * rN * bN, BK = kU * kB;
   const int64_t elem = sp->dtype == OR_F32 ? 4 : 2;
   if ((BM * BK + BK * BN) * elem > 163840) return 0;
-  if (gM * gN > 2147483647LL) return 0;
+  if (gM * gN * 64 * W > 4294967295LL) return 0; /* work-items per dispatch dimension */
   if (kS > 65535) return 0;
   return 1;
 }

@@ -208,10 +208,13 @@ def test_legit_fp32_derived_mfma(orc):
 
 
 def test_legit_grid_limits(orc):
+    # work-items along grid.x = grid_M * grid_N * 64 * waves must stay below 2^32
     sp = orc.Space(65536, 65536, 1, (2, 1, 2), "f32", False)
-    assert not sp.legit(((65536, 1), (1,), (65536, 1), 0))     # 2^32 workgroups
-    assert not sp.legit(((32768, 2), (1,), (65536, 1), 0))     # 2^31 > 2^31 - 1
-    assert sp.legit(((16384, 4), (1,), (65536, 1), 0))         # 2^30
+    assert not sp.legit(((8192, 8), (1,), (8192, 8), 0))       # 2^26 * 64 = 2^32
+    assert sp.legit(((8192, 8), (1,), (4096, 16), 0))          # 2^25 * 64 = 2^31
+    s3 = orc.Space(65536, 65536, 1, (3, 1, 2), "f32", False)
+    assert s3.legit(((4096, 2, 8), (1,), (4096, 16), 0))       # 2^24 * 128 = 2^31
+    assert not s3.legit(((8192, 2, 4), (1,), (4096, 16), 0))   # 2^25 * 128 = 2^32
     sk = orc.Space(1, 1, 131072, (1, 4, 1), "f32", False)
     assert not sk.legit(((1,), (1, 131072, 1, 1), (1,), 0))    # kSplit 2^17 > 65535
     assert sk.legit(((1,), (4, 32768, 1, 1), (1,), 0))
