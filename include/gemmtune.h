@@ -1,0 +1,218 @@
+/*
+ * gemmtune.h — C ABI of libgemmtune: a tiling-parameterised GEMM kernel
+ * family for AMD Instinct MI355X (gfx950) and the Greedy Best-First Search
+ * (G-BFS) that tunes its configuration on the GPU.
+ *
+ * Paper: Compiler-Level Matrix Multiplication Optimization for Deep Learning
+ * (arxiv 1909.10616).
+ *
+ * Conventions for every entry point:
+ *   - Return value: GT_OK (0) or a negative gt_status; gt_last_error() gives a
+ *     thread-local message for the last failure on the calling thread.
+ *   - The caller owns every buffer passed in (host and device). The library
+ *     owns only its kernel attribute cache and the per-search scratch it
+ *     allocates when the caller passes none (freed before tune_gbfs returns).
+ *   - Space functions (gt_space_size … neighbours) are pure host code, need no
+ *     GPU and are thread-safe.
+ *   - Dimension order is m, k, n everywhere, as in the paper's configuration
+ *     (§3.3 Eq.1) and state (§4.1 Eq.5).
+ */
+#ifndef GEMMTUNE_H
+#define GEMMTUNE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define GT_MAXD 4
+
+typedef enum {
+  GT_OK = 0,
+  GT_EINVAL = -1,      /* invalid argument (null pointer, bad enum, bad size) */
+  GT_EDIMS = -2,       /* configuration products do not match M, N, K */
+  GT_EILLEGIT = -3,    /* configuration is not legitimate (J = 0) */
+  GT_EHIP = -4,        /* a HIP runtime call failed */
+  GT_ENOKERNEL = -5,   /* no kernel instantiation for this configuration */
+  GT_ETIMEOUT = -6,    /* search stopped by its time limit before s0 ran */
+  GT_ESMALL = -7       /* output buffer too small; *n_out holds the count */
+} gt_status;
+
+typedef enum { GT_F32 = 0, GT_BF16 = 1 } gt_dtype;
+typedef enum { GT_ADJACENT = 0, GT_ANY_PAIR = 1 } gt_neighbour_mode;
+
+/* Configuration space ξ = ξ_m × ξ_k × ξ_n (§3.3 Eq.1–4).
+ * Each extent D = q·2^E (q odd) is split into d ordered factors, level 0
+ * outermost: level 0 holds q·2^e0, levels ≥ 1 hold powers of two.
+ * mfma_coord = 1 adds the MFMA instruction size {16, 32} as a coordinate.
+ * neighbour_mode: GT_ADJACENT moves a factor of 2 between adjacent levels;
+ * GT_ANY_PAIR between any two levels (§4.1 Eq.6 as printed). */
+typedef struct gt_space {
+  int64_t M, N, K;
+  int32_t d_m, d_k, d_n;   /* 1..GT_MAXD */
+  int32_t dtype;           /* gt_dtype of A and B; C is always fp32 */
+  int32_t mfma_coord;      /* 0 or 1 */
+  int32_t neighbour_mode;  /* gt_neighbour_mode */
+} gt_space;
+
+/* One configuration / state s = [s_m, s_k, s_n, J] (§4.1 Eq.5).
+ * Level meaning (outermost first):
+ *   M, N   d=4 [grid, waves, rep, blk]  d=3 [grid, waves, blk]
+ *          d=2 [grid, blk]               d=1 [grid]
+ *   K      d=4 [kLoop, kSplit, kSub, kBlk]  d=3 [kLoop, kSub, kBlk]
+ *          d=2 [kLoop, kBlk]                d=1 [kLoop]
+ * grid = workgroups along the dimension, waves = wavefronts per workgroup
+ * along it, rep = MFMA blocks per wavefront, blk = block extent; kLoop =
+ * sequential LDS stages, kSplit = workgroups along K, kSub = sub-steps per
+ * stage, kBlk = K elements per sub-step. Unused entries are 0. */
+typedef struct gt_config {
+  int32_t d_m, d_k, d_n;   /* level counts of the space it belongs to */
+  int32_t mfma;            /* 16 or 32 with the coordinate; 0 = derived */
+  int64_t m[GT_MAXD];
+  int64_t k[GT_MAXD];
+  int64_t n[GT_MAXD];
+  int32_t legit;           /* J, written by the functions that return configs */
+  int32_t reserved;
+} gt_config;
+
+/* |ξ| = Π_x C(E_x + d_x − 1, d_x − 1) · (2 if mfma_coord). */
+int gt_space_size(const gt_space* sp, uint64_t* size);
+
+/* Configurations of ranks [start_rank, start_rank + n) in canonical order
+ * (m slowest, then k, n, MFMA 16 before 32; each dimension lexicographic on
+ * its factors), n = min(cap, |ξ| − start_rank). out: caller-owned, cap
+ * entries. Each entry carries J. */
+int enumerate_configs(const gt_space* sp, uint64_t start_rank, gt_config* out,
+                      uint64_t cap, uint64_t* n_out);
+
+/* Rank ↔ configuration bijection with [0, |ξ|). */
+int config_rank(const gt_space* sp, const gt_config* cfg, uint64_t* rank);
+int config_unrank(const gt_space* sp, uint64_t rank, gt_config* cfg);
+
+/* Legitimacy J (§4.1 Eq.5 and its footnote): membership in ξ plus the
+ * hardware predicate — waves ≤ 16; accumulator registers
+ * acc = TM·TN·I²/64 ≤ 256 and acc + 96 ≤ 512/⌈waves/4⌉; LDS stage
+ * (BM·BK + BK·BN)·sizeof(in) ≤ 163840 B; grid_M·grid_N·64·waves ≤ 2^32 − 1;
+ * kSplit ≤ 65535. A non-member gives *J = 0 and GT_OK. */
+int config_legit(const gt_space* sp, const gt_config* cfg, int* J);
+
+/* Neighbour list g(s) = [step(s, a) for a in A] (§4.1 Eq.6, Eq.7, Eq.9) in
+ * ascending rank, illegitimate entries included with legit = 0 (Alg.1
+ * filters them). out: caller-owned, cap entries; too small → GT_ESMALL with
+ * the needed count in *n_out. */
+int neighbours(const gt_space* sp, const gt_config* s, gt_config* out, int cap,
+               int* n_out);
+
+/* C = A·B on the GPU with the kernel the configuration lowers to (§3.2, the
+ * operator being tuned). A: M×K row-major, B: K×N row-major (dtype), C: M×N
+ * row-major fp32, all device pointers. stream: hipStream_t (NULL = default).
+ * Asynchronous; C is overwritten. The configuration's products must equal
+ * M, K, N and it must be legitimate in the space (M, N, K, cfg->d_*, dtype,
+ * mfma_coord = cfg->mfma != 0). */
+int gemm_run(const gt_config* cfg, const void* A, const void* B, void* C,
+             int64_t M, int64_t N, int64_t K, int dtype, void* stream);
+
+/* Cost of one configuration as the search measures it (§4.2 "test", §5 mean
+ * of 10 runs): `warmup` launches (the first one timed on its own), then
+ * `runs` back-to-back launches between two HIP events; *mean_ms = elapsed /
+ * runs. If the first warm-up launch exceeds abort_ms (> 0), timing stops
+ * there, *mean_ms = its time and *aborted = 1. Synchronises the stream. */
+int gt_measure(const gt_config* cfg, const void* A, const void* B, void* C,
+               int64_t M, int64_t N, int64_t K, int dtype, void* stream,
+               int warmup, int runs, double abort_ms, double* mean_ms,
+               double* first_ms, int* aborted);
+
+/* Plain (non-MFMA, one thread per output) GPU product in fp32, used by the
+ * search as the reference its candidates are checked against. Asynchronous. */
+int gt_reference_gemm(const void* A, const void* B, void* C, int64_t M,
+                      int64_t N, int64_t K, int dtype, void* stream);
+
+/* Normwise relative difference max|C − R| / max|R| of two fp32 device
+ * arrays of n elements, computed on the GPU. Synchronises the stream. */
+int gt_compare(const void* C, const void* R, int64_t n, void* stream,
+               double* rel);
+
+/* How a configuration lowers (for reports and tests). */
+typedef struct gt_kernel_info {
+  int32_t I, IK;             /* MFMA instruction size and its K */
+  int32_t TM, TN;            /* MFMA tiles per wavefront */
+  int32_t fast;              /* 1: vectorised swizzled-LDS path */
+  int32_t waves;             /* wavefronts per workgroup */
+  int32_t BM, BN, BK;        /* workgroup tile and LDS stage depth */
+  int32_t dbuf;              /* LDS double buffering */
+  int32_t acc_regs;          /* accumulator registers per lane */
+  int32_t lds_bytes;         /* dynamic LDS per workgroup */
+  int64_t grid_x, grid_y;    /* launch grid (tiles, K splits) */
+} gt_kernel_info;
+int gt_lower(const gt_config* cfg, int64_t M, int64_t N, int64_t K, int dtype,
+             gt_kernel_info* info);
+
+/* ---- G-BFS (§4.2, Alg.1) ---------------------------------------------- */
+
+/* Per-timed-configuration log record. status: 0 ok, 1 early abort,
+ * 2 launch failure (cost +inf), 3 output mismatch (cost +inf). */
+typedef struct gt_log_entry {
+  uint64_t rank;
+  double cost_ms;
+  double first_ms;
+  double rel_err;
+  int32_t status;
+  int32_t reserved;
+} gt_log_entry;
+
+/* Synthetic cost (the CPU "fake backend"): returns the cost of cfg, +inf for
+ * a failure. */
+typedef double (*gt_cost_fn)(const gt_config* cfg, uint64_t rank, void* ctx);
+
+typedef struct gt_tune_opts {
+  const gt_config* s0;   /* NULL: the paper's start state [D,1,…,1], MFMA 16 */
+  int32_t rho;           /* neighbours sampled per pop (ρ); default 5 */
+  int32_t runs;          /* timed runs per configuration; default 10 */
+  int32_t warmup;        /* untimed-for-cost warm-up launches; default 1 */
+  int32_t check;         /* 1: compare every timed output with the reference */
+  int64_t budget;        /* configurations timed, s0 included; ≥ 1 */
+  double t_max_s;        /* search time limit in seconds; 0 = none */
+  uint64_t seed;         /* SplitMix64 seed of the ρ-sampling */
+  double max_run_ms;     /* early abort when the warm-up exceeds this; 250 */
+  double abort_factor;   /* … or exceeds abort_factor · cost_min; 50 */
+  /* GPU mode (cost callback NULL): device buffers and stream. */
+  const void* A;
+  const void* B;
+  void* C;
+  void* c_ref;           /* M·N fp32 scratch for the reference; NULL: allocated */
+  void* stream;
+  gt_log_entry* log;     /* optional, caller-owned, log_cap entries */
+  int64_t log_cap;
+} gt_tune_opts;
+
+typedef struct gt_tune_result {
+  gt_config best;        /* s* */
+  uint64_t best_rank;
+  double best_cost;      /* cost_min (ms in GPU mode) */
+  int64_t timed;         /* configurations timed (≤ budget) */
+  int64_t popped;
+  int64_t skipped_illegit;
+  int64_t skipped_visited;
+  int64_t failed;        /* timed with cost +inf */
+  double wall_s;
+  int32_t stop_reason;   /* 0 budget, 1 queue empty, 2 time limit */
+  int32_t reserved;
+} gt_tune_result;
+
+/* Fills the defaults listed in gt_tune_opts (budget 1000, seed 0). */
+int gt_tune_opts_init(gt_tune_opts* opts);
+
+/* G-BFS over the space. cost == NULL times gemm_run on the GPU with
+ * opts->A/B/C/stream (and checks outputs when opts->check); otherwise
+ * cost(cfg, rank, ctx) is called for every timed configuration. */
+int tune_gbfs(const gt_space* sp, const gt_tune_opts* opts, gt_cost_fn cost,
+              void* ctx, gt_tune_result* out);
+
+/* Thread-local message of the last failure. */
+const char* gt_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GEMMTUNE_H */

@@ -1,0 +1,82 @@
+"""Build libgemmtune.so (HIP, gfx950) in-tree.
+
+Every source is compiled with hipcc for gfx950 into ``_build/`` in parallel
+and linked into ``paper_1909_10616_amd/_lib/libgemmtune.so``. The kernel
+family is split into one translation unit per (dtype, MFMA size, path).
+"""
+from __future__ import annotations
+
+import concurrent.futures as cf
+import os
+import shutil
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+BUILD = os.path.join(ROOT, "_build")
+LIBDIR = os.path.join(PKG, "_lib")
+LIB = os.path.join(LIBDIR, "libgemmtune.so")
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+ARCH = "gfx950"
+
+COMMON = [
+    "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
+    # packed fp32 vector ops stay off on this target
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-munsafe-fp-atomics",
+    "-I", os.path.join(ROOT, "include"), "-I", CSRC,
+]
+
+
+def _units():
+    units = [
+        ("space", "space.cpp", []),
+        ("search", "search.cpp", []),
+        ("runtime", "runtime.cpp", []),
+        ("aux_kernels", "aux_kernels.hip", []),
+    ]
+    for dt, dn in ((0, "f32"), (1, "bf16")):
+        for i in (16, 32):
+            for fast, pn in ((0, "generic"), (1, "fast")):
+                units.append((f"gemm_{dn}_{i}_{pn}", "gemm_inst.hip",
+                              [f"-DGT_DT={dt}", f"-DGT_I={i}", f"-DGT_FAST={fast}"]))
+    return units
+
+
+def _compile(unit):
+    name, src, defs = unit
+    obj = os.path.join(BUILD, name + ".o")
+    cmd = [HIPCC, *COMMON, "-x", "hip", *defs, "-c", os.path.join(CSRC, src), "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    err = "\n".join(l for l in r.stderr.splitlines() if "packed-fp32-ops" not in l)
+    if r.returncode != 0:
+        raise RuntimeError(f"compile {name} failed:\n{err}")
+    return obj
+
+
+def build(jobs: int | None = None, verbose: bool = True) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    os.makedirs(LIBDIR, exist_ok=True)
+    jobs = jobs or min(16, os.cpu_count() or 4)
+    units = _units()
+    with cf.ThreadPoolExecutor(max_workers=jobs) as ex:
+        objs = list(ex.map(_compile, units))
+    tmp = LIB + ".tmp"
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("link failed:\n" + r.stderr)
+    os.replace(tmp, LIB)
+    if verbose:
+        print(f"built {LIB}", file=sys.stderr)
+    return LIB
+
+
+def clean():
+    shutil.rmtree(BUILD, ignore_errors=True)
+
+
+if __name__ == "__main__":
+    build()

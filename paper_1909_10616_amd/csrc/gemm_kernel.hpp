@@ -1,0 +1,551 @@
+// Tiling-parameterised GEMM kernel family for gfx950 (CDNA4).
+//
+// C (M×N, fp32, row-major) = A (M×K, row-major) · B (K×N, row-major), the
+// operator whose loop-tiling configuration the search tunes (§3.2, §3.3).
+// A configuration's levels map to the launch as follows (level 0 outermost):
+//   rows    = ((gridM·wavesM + wm)·repM + rep)·blkM + b
+//   k index = ((kLoop·kSplit + z)·kSub + s)·kBlk + b
+// Compile-time parameters: input dtype, MFMA size I (16/32), MFMA tiles per
+// wavefront TM × TN, and the path:
+//   generic — any legitimate configuration; blocks smaller than the MFMA
+//             instruction are zero-padded in registers, LDS holds the natural
+//             row-major tiles;
+//   fast    — blocks that are multiples of the instruction: 16-byte global
+//             loads staged through registers one stage ahead, B transposed in
+//             registers so every LDS fragment read is one 16-byte read, LDS
+//             tiles XOR-swizzled by 128-byte line to avoid bank conflicts.
+// Everything else (grid, waves, block extents, stage depth, split-K, double
+// buffering) is a runtime argument.
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace gt {
+
+struct KArgs {
+  const void* A;
+  const void* B;
+  float* C;
+  int64_t M, N, K;
+  int32_t gridM, gridN;
+  int32_t wavesM, wavesN;
+  int32_t blkM, blkN;
+  int32_t lgTpbM, lgTpbN;  // log2 of MFMA tiles per block (blk ≥ I) else 0
+  int32_t kLoop, kSplit, kSub, kBlk;
+  int32_t BM, BN, BK;
+  int32_t WM, WN;          // wavefront tile
+  int32_t lgBK, lgBN;
+  int32_t dbuf;
+  int32_t atomic;          // split-K: accumulate with fp32 atomics
+  int32_t remap;           // XCD-aware workgroup order
+  int32_t aVec, bVec;      // generic path: 1 or 16-byte vector tile loads
+};
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+
+template <int DT>
+struct Elem;
+template <>
+struct Elem<0> {  // fp32
+  using T = float;
+  static constexpr int VEC = 4;  // elements per 16-byte chunk
+  static constexpr int EPL = 1;  // elements per lane per MFMA operand
+};
+template <>
+struct Elem<1> {  // bf16 (stored as raw 16-bit patterns)
+  using T = uint16_t;
+  static constexpr int VEC = 8;
+  static constexpr int EPL = 8;
+};
+
+template <int I>
+struct AccT;
+template <>
+struct AccT<32> {
+  using type = f32x16;
+  static constexpr int N = 16;
+};
+template <>
+struct AccT<16> {
+  using type = f32x4;
+  static constexpr int N = 4;
+};
+
+// Row (inside the I×I output tile) of accumulator element i held by lane;
+// the column is lane % I.
+template <int I>
+__device__ __forceinline__ int out_row(int lane, int i) {
+  if constexpr (I == 32)
+    return 8 * (i >> 2) + 4 * (lane >> 5) + (i & 3);
+  else
+    return 4 * (lane >> 4) + i;
+}
+
+__device__ __forceinline__ f32x16 mfma_bf16(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma_bf16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x16 mfma_f32(float a, float b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4 mfma_f32(float a, float b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+}
+
+// Workgroup → (tile row, tile column). Consecutive workgroups are dispatched
+// round-robin over the 8 XCDs; with `remap` each XCD receives a contiguous
+// run of tiles, ordered in groups of 4 tile rows so that the tiles sharing
+// an XCD's L2 share A row-blocks and B column-blocks.
+__device__ __forceinline__ void tile_of(const KArgs& a, int& gm, int& gn) {
+  const int nt = a.gridM * a.gridN;
+  int t = static_cast<int>(blockIdx.x);
+  if (a.remap) t = (t & 7) * (nt >> 3) + (t >> 3);
+  constexpr int G = 4;
+  const int per_group = G * a.gridN;
+  const int group = t / per_group;
+  const int first = group * G;
+  const int gsize = min(a.gridM - first, G);
+  const int r = t - group * per_group;
+  gm = first + r % gsize;
+  gn = r / gsize;
+}
+
+__device__ __forceinline__ void put(bool atomic, float* p, float v) {
+  if (atomic)
+    unsafeAtomicAdd(p, v);
+  else
+    *p = v;
+}
+
+// ---------------------------------------------------------------------------
+// Generic path
+// ---------------------------------------------------------------------------
+
+template <typename T, int VEC>
+__device__ __forceinline__ void copy_tile(T* lds, const T* g, int64_t ld, int rows, int cols,
+                                          int lgcols, int vec, int tid, int nthr) {
+  if (vec > 1) {
+    constexpr int LGV = VEC == 8 ? 3 : 2;
+    const int lgcpr = lgcols - LGV;
+    const int chunks = (rows * cols) >> LGV;
+    for (int e = tid; e < chunks; e += nthr) {
+      const int r = e >> lgcpr;
+      const int c = (e & ((1 << lgcpr) - 1)) << LGV;
+      *reinterpret_cast<uint4*>(lds + (r << lgcols) + c) =
+          *reinterpret_cast<const uint4*>(g + r * ld + c);
+    }
+  } else {
+    const int total = rows * cols;
+    for (int e = tid; e < total; e += nthr) {
+      const int r = e >> lgcols;
+      const int c = e & (cols - 1);
+      lds[e] = g[r * ld + c];
+    }
+  }
+}
+
+template <int DT, int I, int TM, int TN>
+__device__ void gemm_generic(const KArgs& a, char* smem) {
+  using T = typename Elem<DT>::T;
+  using acc_t = typename AccT<I>::type;
+  constexpr int NACC = AccT<I>::N;
+  constexpr int EPL = Elem<DT>::EPL;
+  constexpr int G = 64 / I;
+  constexpr int IK = EPL * G;
+  const int tid = threadIdx.x;
+  const int nthr = blockDim.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave % a.wavesM;
+  const int wn = wave / a.wavesM;
+  int gm, gn;
+  tile_of(a, gm, gn);
+  const int z = blockIdx.y;
+
+  T* As0 = reinterpret_cast<T*>(smem);
+  const int stage = (a.BM + a.BN) * a.BK;
+  const T* Ag = reinterpret_cast<const T*>(a.A) + static_cast<int64_t>(gm) * a.BM * a.K;
+  const T* Bg = reinterpret_cast<const T*>(a.B) + static_cast<int64_t>(gn) * a.BN;
+
+  // Rows of A / columns of B this lane feeds into each MFMA tile.
+  int arow[TM], bcol[TN];
+  bool aok[TM], bok[TN];
+  const int tpbM = 1 << a.lgTpbM, tpbN = 1 << a.lgTpbN;
+#pragma unroll
+  for (int t = 0; t < TM; ++t) {
+    const int in = (t & (tpbM - 1)) * I + (lane % I);
+    aok[t] = in < a.blkM;
+    arow[t] = wm * a.WM + (t >> a.lgTpbM) * a.blkM + in;
+  }
+#pragma unroll
+  for (int t = 0; t < TN; ++t) {
+    const int in = (t & (tpbN - 1)) * I + (lane % I);
+    bok[t] = in < a.blkN;
+    bcol[t] = wn * a.WN + (t >> a.lgTpbN) * a.blkN + in;
+  }
+
+  acc_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = acc_t{};
+
+  auto load_stage = [&](int l, int buf) {
+    const int64_t kbase = (static_cast<int64_t>(l) * a.kSplit + z) * a.BK;
+    T* as = As0 + buf * stage;
+    T* bs = as + a.BM * a.BK;
+    copy_tile<T, Elem<DT>::VEC>(as, Ag + kbase, a.K, a.BM, a.BK, a.lgBK, a.aVec, tid, nthr);
+    copy_tile<T, Elem<DT>::VEC>(bs, Bg + kbase * a.N, a.N, a.BK, a.BN, a.lgBN, a.bVec, tid, nthr);
+  };
+
+  auto compute = [&](int buf) {
+    const T* as = As0 + buf * stage;
+    const T* bs = as + a.BM * a.BK;
+    const int nkk = (a.kBlk + IK - 1) / IK;
+    for (int s = 0; s < a.kSub; ++s) {
+      for (int kk = 0; kk < nkk; ++kk) {
+        const int kl0 = kk * IK + (lane / I) * EPL;  // this lane's first k in the sub-step
+        if constexpr (DT == 1) {
+          bf16x8 af[TM], bfv[TN];
+#pragma unroll
+          for (int t = 0; t < TM; ++t) {
+            uint16_t v[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const int kl = kl0 + e;
+              v[e] = (aok[t] && kl < a.kBlk) ? as[arow[t] * a.BK + s * a.kBlk + kl] : uint16_t(0);
+            }
+            af[t] = __builtin_bit_cast(bf16x8, v);
+          }
+#pragma unroll
+          for (int t = 0; t < TN; ++t) {
+            uint16_t v[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const int kl = kl0 + e;
+              v[e] = (bok[t] && kl < a.kBlk) ? bs[(s * a.kBlk + kl) * a.BN + bcol[t]] : uint16_t(0);
+            }
+            bfv[t] = __builtin_bit_cast(bf16x8, v);
+          }
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] = mfma_bf16(af[i], bfv[j], acc[i][j]);
+        } else {
+          float af[TM], bfv[TN];
+          const bool kin = kl0 < a.kBlk;
+#pragma unroll
+          for (int t = 0; t < TM; ++t)
+            af[t] = (aok[t] && kin) ? as[arow[t] * a.BK + s * a.kBlk + kl0] : 0.0f;
+#pragma unroll
+          for (int t = 0; t < TN; ++t)
+            bfv[t] = (bok[t] && kin) ? bs[(s * a.kBlk + kl0) * a.BN + bcol[t]] : 0.0f;
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j) acc[i][j] = mfma_f32(af[i], bfv[j], acc[i][j]);
+        }
+      }
+    }
+  };
+
+  load_stage(0, 0);
+  __syncthreads();
+  for (int l = 0; l < a.kLoop; ++l) {
+    const int cur = a.dbuf ? (l & 1) : 0;
+    const bool next = l + 1 < a.kLoop;
+    if (a.dbuf && next) load_stage(l + 1, cur ^ 1);
+    compute(cur);
+    __syncthreads();
+    if (!a.dbuf && next) {
+      load_stage(l + 1, 0);
+      __syncthreads();
+    }
+  }
+
+  float* Cw = a.C + static_cast<int64_t>(gm) * a.BM * a.N + static_cast<int64_t>(gn) * a.BN;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+#pragma unroll
+      for (int e = 0; e < NACC; ++e) {
+        const int ri = (i & (tpbM - 1)) * I + out_row<I>(lane, e);
+        const int ci = (j & (tpbN - 1)) * I + (lane % I);
+        if (ri < a.blkM && ci < a.blkN) {
+          const int r = wm * a.WM + (i >> a.lgTpbM) * a.blkM + ri;
+          const int c = wn * a.WN + (j >> a.lgTpbN) * a.blkN + ci;
+          put(a.atomic != 0, Cw + static_cast<int64_t>(r) * a.N + c, acc[i][j][e]);
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Fast path
+// ---------------------------------------------------------------------------
+
+// 16-byte chunk q of a tile → its LDS slot: XOR inside each 128-byte line
+// (8 chunks) with a hash of the line index, so that the 8 or 16 lanes served
+// together by a 16-byte LDS read hit distinct banks.
+__device__ __forceinline__ int swz(int q) { return q ^ (((q >> 3) ^ (q >> 6)) & 7); }
+
+constexpr int kPfA = 8;  // A chunks staged in registers per thread
+constexpr int kPfB = 1;  // B VEC×VEC blocks staged per thread
+
+// Transpose a VEC×VEC block held as VEC row chunks into VEC column chunks.
+template <int DT>
+__device__ __forceinline__ void transpose_block(const uint4* in, uint4* out) {
+  if constexpr (DT == 1) {
+    // 8×8 of 16-bit values; dword w of a chunk holds elements 2w (low), 2w+1 (high)
+    const uint32_t* r = reinterpret_cast<const uint32_t*>(in);  // r[j*4 + w]
+    uint32_t* o = reinterpret_cast<uint32_t*>(out);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const uint32_t lo = r[(2 * w) * 4 + u], hi = r[(2 * w + 1) * 4 + u];
+        o[(2 * u) * 4 + w] = (lo & 0xffffu) | (hi << 16);
+        o[(2 * u + 1) * 4 + w] = (lo >> 16) | (hi & 0xffff0000u);
+      }
+    }
+  } else {
+    const float* r = reinterpret_cast<const float*>(in);
+    float* o = reinterpret_cast<float*>(out);
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) o[t * 4 + j] = r[j * 4 + t];
+  }
+}
+
+template <int DT, int I, int TM, int TN>
+__device__ void gemm_fast(const KArgs& a, char* smem) {
+  using T = typename Elem<DT>::T;
+  using acc_t = typename AccT<I>::type;
+  constexpr int NACC = AccT<I>::N;
+  constexpr int VEC = Elem<DT>::VEC;
+  constexpr int LGV = VEC == 8 ? 3 : 2;
+  constexpr int G = 64 / I;
+  const int tid = threadIdx.x;
+  const int nthr = blockDim.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave % a.wavesM;
+  const int wn = wave / a.wavesM;
+  int gm, gn;
+  tile_of(a, gm, gn);
+  const int z = blockIdx.y;
+
+  const int lgcpr = a.lgBK - LGV;  // chunks per row = BK / VEC
+  const int cpr = 1 << lgcpr;
+  const int achunks = a.BM << lgcpr;
+  const int nbk = a.BK >> LGV, nbn = a.BN >> LGV;  // B blocks along k and n
+  const int bblocks = nbk * nbn;
+  const int stage = achunks + (a.BN << lgcpr);  // chunks per stage
+  uint4* lds = reinterpret_cast<uint4*>(smem);
+
+  const T* Ag = reinterpret_cast<const T*>(a.A) + static_cast<int64_t>(gm) * a.BM * a.K;
+  const T* Bg = reinterpret_cast<const T*>(a.B) + static_cast<int64_t>(gn) * a.BN;
+
+  const int rounds = max((achunks + nthr * kPfA - 1) / (nthr * kPfA),
+                         (bblocks + nthr * kPfB - 1) / (nthr * kPfB));
+  const bool prefetch = rounds == 1;
+
+  uint4 ra[kPfA];
+  uint4 rb[kPfB * VEC];
+
+  auto gload = [&](int l, int round) {
+    const int64_t kbase = (static_cast<int64_t>(l) * a.kSplit + z) * a.BK;
+#pragma unroll
+    for (int i = 0; i < kPfA; ++i) {
+      const int e = tid + (round * kPfA + i) * nthr;
+      if (e < achunks) {
+        const int r = e >> lgcpr, c = e & (cpr - 1);
+        ra[i] = *reinterpret_cast<const uint4*>(Ag + r * a.K + kbase + (c << LGV));
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < kPfB; ++i) {
+      const int b = tid + (round * kPfB + i) * nthr;
+      if (b < bblocks) {
+        const int nb = b % nbn, kb = b / nbn;
+        const T* src = Bg + (kbase + (kb << LGV)) * a.N + (nb << LGV);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) rb[i * VEC + j] = *reinterpret_cast<const uint4*>(src + j * a.N);
+      }
+    }
+  };
+
+  auto lstore = [&](int buf, int round) {
+    uint4* as = lds + buf * stage;
+    uint4* bs = as + achunks;
+#pragma unroll
+    for (int i = 0; i < kPfA; ++i) {
+      const int e = tid + (round * kPfA + i) * nthr;
+      if (e < achunks) as[swz(e)] = ra[i];
+    }
+#pragma unroll
+    for (int i = 0; i < kPfB; ++i) {
+      const int b = tid + (round * kPfB + i) * nthr;
+      if (b < bblocks) {
+        const int nb = b % nbn, kb = b / nbn;
+        uint4 t[VEC];
+        transpose_block<DT>(&rb[i * VEC], t);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) bs[swz((((nb << LGV) + j) << lgcpr) + kb)] = t[j];
+      }
+    }
+  };
+
+  acc_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = acc_t{};
+
+  const int arow0 = wm * a.WM + (lane % I);
+  const int bcol0 = wn * a.WN + (lane % I);
+  const int grp = lane / I;
+
+  auto compute = [&](int buf) {
+    const uint4* as = lds + buf * stage;
+    const uint4* bs = as + achunks;
+    const int ncs = cpr / G;
+    for (int cs = 0; cs < ncs; ++cs) {
+      const int ch = cs * G + grp;
+      uint4 af[TM], bfv[TN];
+#pragma unroll
+      for (int t = 0; t < TM; ++t) af[t] = as[swz(((arow0 + t * I) << lgcpr) + ch)];
+#pragma unroll
+      for (int t = 0; t < TN; ++t) bfv[t] = bs[swz(((bcol0 + t * I) << lgcpr) + ch)];
+      if constexpr (DT == 1) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+          for (int j = 0; j < TN; ++j)
+            acc[i][j] = mfma_bf16(__builtin_bit_cast(bf16x8, af[i]),
+                                  __builtin_bit_cast(bf16x8, bfv[j]), acc[i][j]);
+      } else {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+          for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+              acc[i][j] = mfma_f32(__builtin_bit_cast(f32x4, af[i])[q],
+                                   __builtin_bit_cast(f32x4, bfv[j])[q], acc[i][j]);
+      }
+    }
+  };
+
+  if (prefetch) {
+    gload(0, 0);
+    lstore(0, 0);
+  } else {
+    for (int r = 0; r < rounds; ++r) {
+      gload(0, r);
+      lstore(0, r);
+    }
+  }
+  __syncthreads();
+  for (int l = 0; l < a.kLoop; ++l) {
+    const int cur = a.dbuf ? (l & 1) : 0;
+    const bool next = l + 1 < a.kLoop;
+    if (prefetch && next) gload(l + 1, 0);
+    compute(cur);
+    if (next) {
+      if (!a.dbuf) __syncthreads();
+      const int nxt = a.dbuf ? (cur ^ 1) : 0;
+      if (prefetch) {
+        lstore(nxt, 0);
+      } else {
+        for (int r = 0; r < rounds; ++r) {
+          gload(l + 1, r);
+          lstore(nxt, r);
+        }
+      }
+      __syncthreads();
+    }
+  }
+
+  float* Cw = a.C + static_cast<int64_t>(gm) * a.BM * a.N + static_cast<int64_t>(gn) * a.BN;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+#pragma unroll
+      for (int e = 0; e < NACC; ++e) {
+        const int r = wm * a.WM + i * I + out_row<I>(lane, e);
+        const int c = wn * a.WN + j * I + (lane % I);
+        put(a.atomic != 0, Cw + static_cast<int64_t>(r) * a.N + c, acc[i][j][e]);
+      }
+    }
+  }
+}
+
+// Launch bound: the largest wavefront count the legitimacy rule admits for
+// this accumulator size (acc + 96 ≤ 512 / ⌈waves/4⌉); the fast path is used
+// with at most 8 wavefronts.
+template <int I, int TM, int TN>
+constexpr int max_waves() {
+  constexpr int acc = TM * TN * I * I / 64;
+  return acc + 96 <= 128 ? 16 : (acc + 96 <= 256 ? 8 : 4);
+}
+
+template <int DT, int I, int TM, int TN, bool FAST>
+__global__ void __launch_bounds__(64 * (FAST ? (max_waves<I, TM, TN>() > 8 ? 8 : max_waves<I, TM, TN>())
+                                              : max_waves<I, TM, TN>()))
+    gemm_kernel(KArgs a) {
+  extern __shared__ uint4 gt_smem[];
+  char* smem = reinterpret_cast<char*>(gt_smem);
+  if constexpr (FAST)
+    gemm_fast<DT, I, TM, TN>(a, smem);
+  else
+    gemm_generic<DT, I, TM, TN>(a, smem);
+}
+
+using LaunchFn = hipError_t (*)(const KArgs&, dim3, dim3, size_t, hipStream_t);
+
+template <int DT, int I, int TM, int TN, bool FAST>
+hipError_t launch_gemm(const KArgs& a, dim3 grid, dim3 block, size_t lds, hipStream_t s) {
+  auto fn = gemm_kernel<DT, I, TM, TN, FAST>;
+  static bool attr_set = false;  // raise the dynamic LDS limit once per kernel
+  if (!attr_set) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 163840);
+    if (e != hipSuccess) return e;
+    attr_set = true;
+  }
+  hipLaunchKernelGGL(fn, grid, block, lds, s, a);
+  return hipGetLastError();
+}
+
+// (TM, TN) pairs with TM·TN ≤ 16 (I = 32) and ≤ 64 (I = 16): the register
+// rule acc = TM·TN·I²/64 ≤ 256.
+#define GT_PAIRS_16(X)                                                                      \
+  X(1, 1) X(1, 2) X(2, 1) X(1, 4) X(2, 2) X(4, 1) X(1, 8) X(2, 4) X(4, 2) X(8, 1) X(1, 16) \
+      X(2, 8) X(4, 4) X(8, 2) X(16, 1)
+#define GT_PAIRS_64(X)                                                                       \
+  GT_PAIRS_16(X)                                                                             \
+  X(1, 32) X(2, 16) X(4, 8) X(8, 4) X(16, 2) X(32, 1) X(1, 64) X(2, 32) X(4, 16) X(8, 8)     \
+      X(16, 4) X(32, 2) X(64, 1)
+
+// Lookup of one translation unit: (TM, TN) → launcher, or nullptr.
+using LookupFn = LaunchFn (*)(int, int);
+LaunchFn lookup_f32_16_generic(int, int);
+LaunchFn lookup_f32_32_generic(int, int);
+LaunchFn lookup_bf16_16_generic(int, int);
+LaunchFn lookup_bf16_32_generic(int, int);
+LaunchFn lookup_f32_16_fast(int, int);
+LaunchFn lookup_f32_32_fast(int, int);
+LaunchFn lookup_bf16_16_fast(int, int);
+LaunchFn lookup_bf16_32_fast(int, int);
+
+}  // namespace gt

@@ -1,0 +1,319 @@
+// Lowering of a configuration to a kernel launch, the GEMM entry point, the
+// cost measurement the search uses (§4.2 "test" a configuration on the
+// hardware; §5: cost is the mean of 10 runs), and the reference/compare
+// helpers.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <mutex>
+#include <string>
+
+#include "aux_kernels.h"
+#include "gemm_kernel.hpp"
+#include "internal.h"
+#include "runtime.h"
+
+namespace gt {
+
+namespace {
+
+int ilog2(int64_t v) {
+  int e = 0;
+  while ((int64_t{1} << e) < v) ++e;
+  return e;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+LaunchFn find_kernel(int dtype, int I, bool fast, int TM, int TN) {
+  if (dtype == GT_F32) {
+    if (I == 16) return fast ? lookup_f32_16_fast(TM, TN) : lookup_f32_16_generic(TM, TN);
+    return fast ? lookup_f32_32_fast(TM, TN) : lookup_f32_32_generic(TM, TN);
+  }
+  if (I == 16) return fast ? lookup_bf16_16_fast(TM, TN) : lookup_bf16_16_generic(TM, TN);
+  return fast ? lookup_bf16_32_fast(TM, TN) : lookup_bf16_32_generic(TM, TN);
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  set_error(std::string(what) + ": " + hipGetErrorString(e));
+  return GT_EHIP;
+}
+
+}  // namespace
+
+int lower(const gt_config& c, int64_t M, int64_t N, int64_t K, int dtype, const void* A,
+          const void* B, void* C, Lowered* out) {
+  gt_space sp{};
+  sp.M = M;
+  sp.N = N;
+  sp.K = K;
+  sp.d_m = c.d_m;
+  sp.d_k = c.d_k;
+  sp.d_n = c.d_n;
+  sp.dtype = dtype;
+  sp.mfma_coord = c.mfma != 0 ? 1 : 0;
+  sp.neighbour_mode = GT_ADJACENT;
+  Space s;
+  if (int rc = make_space(&sp, &s)) return rc;
+  if (!is_member(s, c)) {
+    set_error("configuration does not factor M, K, N (or bad MFMA value)");
+    return GT_EDIMS;
+  }
+  if (!legit_of(s, c)) {
+    set_error("configuration is not legitimate (J = 0)");
+    return GT_EILLEGIT;
+  }
+  Levels& L = out->L;
+  levels_of(c, dtype, &L);
+  const int vec = dtype == GT_BF16 ? 8 : 4;
+  const int G = 64 / L.I;
+  const bool fast = L.blkM % L.I == 0 && L.blkN % L.I == 0 && L.kBlk % L.IK == 0 &&
+                    L.BK % (vec * G) == 0 && L.BN % vec == 0 && K % vec == 0 && N % vec == 0 &&
+                    L.W <= 8 && aligned16(A) && aligned16(B);
+  const int64_t stage_bytes = (L.BM * L.BK + L.BK * L.BN) * L.elem;
+  const bool dbuf = L.kLoop >= 2 && 2 * stage_bytes <= kLdsMax;
+
+  KArgs& a = out->args;
+  std::memset(&a, 0, sizeof(a));
+  a.A = A;
+  a.B = B;
+  a.C = static_cast<float*>(C);
+  a.M = M;
+  a.N = N;
+  a.K = K;
+  a.gridM = static_cast<int32_t>(L.gridM);
+  a.gridN = static_cast<int32_t>(L.gridN);
+  a.wavesM = static_cast<int32_t>(L.wavesM);
+  a.wavesN = static_cast<int32_t>(L.wavesN);
+  a.blkM = static_cast<int32_t>(L.blkM);
+  a.blkN = static_cast<int32_t>(L.blkN);
+  a.lgTpbM = L.blkM >= L.I ? ilog2(L.blkM / L.I) : 0;
+  a.lgTpbN = L.blkN >= L.I ? ilog2(L.blkN / L.I) : 0;
+  a.kLoop = static_cast<int32_t>(L.kLoop);
+  a.kSplit = static_cast<int32_t>(L.kSplit);
+  a.kSub = static_cast<int32_t>(L.kSub);
+  a.kBlk = static_cast<int32_t>(L.kBlk);
+  a.BM = static_cast<int32_t>(L.BM);
+  a.BN = static_cast<int32_t>(L.BN);
+  a.BK = static_cast<int32_t>(L.BK);
+  a.WM = static_cast<int32_t>(L.repM * L.blkM);
+  a.WN = static_cast<int32_t>(L.repN * L.blkN);
+  a.lgBK = ilog2(L.BK);
+  a.lgBN = ilog2(L.BN);
+  a.dbuf = dbuf ? 1 : 0;
+  a.atomic = L.kSplit > 1 ? 1 : 0;
+  a.remap = (L.gridM * L.gridN) % 8 == 0 ? 1 : 0;
+  a.aVec = (L.BK % vec == 0 && K % vec == 0 && aligned16(A)) ? vec : 1;
+  a.bVec = (L.BN % vec == 0 && N % vec == 0 && aligned16(B)) ? vec : 1;
+
+  out->grid = dim3(static_cast<unsigned>(L.gridM * L.gridN), static_cast<unsigned>(L.kSplit), 1);
+  out->block = dim3(static_cast<unsigned>(64 * L.W), 1, 1);
+  out->lds = static_cast<size_t>(stage_bytes * (dbuf ? 2 : 1));
+  out->fast = fast;
+  out->fn = find_kernel(dtype, L.I, fast, static_cast<int>(L.TM), static_cast<int>(L.TN));
+  if (!out->fn) {
+    set_error("no kernel instantiation for this MFMA tile shape");
+    return GT_ENOKERNEL;
+  }
+  return GT_OK;
+}
+
+int launch_lowered(const Lowered& lw, hipStream_t s) {
+  if (lw.args.atomic) {
+    hipError_t e = launch_fill_zero(lw.args.C, lw.args.M * lw.args.N, s);
+    if (e != hipSuccess) return hip_fail(e, "clearing C for split-K");
+  }
+  hipError_t e = lw.fn(lw.args, lw.grid, lw.block, lw.lds, s);
+  if (e != hipSuccess) return hip_fail(e, "GEMM launch");
+  return GT_OK;
+}
+
+namespace {
+std::mutex g_cmp_mu;
+unsigned* g_cmp_buf[64] = {};  // per device, 2 words, kept until process exit
+}  // namespace
+
+int compare_on_gpu(const void* C, const void* R, int64_t n, hipStream_t s, double* rel) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= 64) {
+    set_error("device index out of range");
+    return GT_EINVAL;
+  }
+  unsigned* buf;
+  {
+    std::lock_guard<std::mutex> lk(g_cmp_mu);
+    if (!g_cmp_buf[dev]) {
+      e = hipMalloc(&g_cmp_buf[dev], 2 * sizeof(unsigned));
+      if (e != hipSuccess) return hip_fail(e, "hipMalloc (compare result)");
+    }
+    buf = g_cmp_buf[dev];
+  }
+  e = launch_compare(static_cast<const float*>(C), static_cast<const float*>(R), n, buf, s);
+  if (e != hipSuccess) return hip_fail(e, "compare launch");
+  unsigned host[2];
+  e = hipMemcpyAsync(host, buf, sizeof(host), hipMemcpyDeviceToHost, s);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (compare result)");
+  e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize (compare)");
+  float md, mr;
+  std::memcpy(&md, &host[0], 4);
+  std::memcpy(&mr, &host[1], 4);
+  if (std::isnan(md))
+    *rel = NAN;
+  else if (mr == 0.0f)
+    *rel = md == 0.0f ? 0.0 : INFINITY;
+  else
+    *rel = static_cast<double>(md) / static_cast<double>(mr);
+  return GT_OK;
+}
+
+int measure(const gt_config& c, const void* A, const void* B, void* C, int64_t M, int64_t N,
+            int64_t K, int dtype, hipStream_t s, int warmup, int runs, double abort_ms,
+            double* mean_ms, double* first_ms, int* aborted) {
+  Lowered lw;
+  if (int rc = lower(c, M, N, K, dtype, A, B, C, &lw)) return rc;
+  hipEvent_t ev[4];
+  for (auto& x : ev) {
+    hipError_t e = hipEventCreate(&x);
+    if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+  }
+  auto destroy = [&]() {
+    for (auto& x : ev) hipEventDestroy(x);
+  };
+  int rc = GT_OK;
+  float first = 0.0f, total = 0.0f;
+  *aborted = 0;
+  hipError_t e;
+  if (warmup < 1) warmup = 1;
+  if (runs < 1) runs = 1;
+  // first warm-up launch, timed on its own for the early-abort rule
+  if ((e = hipEventRecord(ev[0], s)) != hipSuccess) {
+    destroy();
+    return hip_fail(e, "hipEventRecord");
+  }
+  if ((rc = launch_lowered(lw, s)) != GT_OK) {
+    hipStreamSynchronize(s);
+    destroy();
+    return rc;
+  }
+  hipEventRecord(ev[1], s);
+  if ((e = hipEventSynchronize(ev[1])) != hipSuccess) {
+    destroy();
+    return hip_fail(e, "warm-up run");
+  }
+  hipEventElapsedTime(&first, ev[0], ev[1]);
+  *first_ms = first;
+  if (abort_ms > 0.0 && first > abort_ms) {
+    *aborted = 1;
+    *mean_ms = first;
+    destroy();
+    return GT_OK;
+  }
+  for (int w = 1; w < warmup; ++w)
+    if ((rc = launch_lowered(lw, s)) != GT_OK) {
+      destroy();
+      return rc;
+    }
+  hipEventRecord(ev[2], s);
+  for (int r = 0; r < runs; ++r)
+    if ((rc = launch_lowered(lw, s)) != GT_OK) {
+      hipStreamSynchronize(s);
+      destroy();
+      return rc;
+    }
+  hipEventRecord(ev[3], s);
+  if ((e = hipEventSynchronize(ev[3])) != hipSuccess) {
+    destroy();
+    return hip_fail(e, "timed runs");
+  }
+  hipEventElapsedTime(&total, ev[2], ev[3]);
+  *mean_ms = static_cast<double>(total) / runs;
+  destroy();
+  return GT_OK;
+}
+
+}  // namespace gt
+
+extern "C" {
+
+int gemm_run(const gt_config* cfg, const void* A, const void* B, void* C, int64_t M, int64_t N,
+             int64_t K, int dtype, void* stream) {
+  if (!cfg || !A || !B || !C) {
+    gt::set_error("gemm_run: null argument");
+    return GT_EINVAL;
+  }
+  gt::Lowered lw;
+  if (int rc = gt::lower(*cfg, M, N, K, dtype, A, B, C, &lw)) return rc;
+  return gt::launch_lowered(lw, static_cast<hipStream_t>(stream));
+}
+
+int gt_measure(const gt_config* cfg, const void* A, const void* B, void* C, int64_t M, int64_t N,
+               int64_t K, int dtype, void* stream, int warmup, int runs, double abort_ms,
+               double* mean_ms, double* first_ms, int* aborted) {
+  if (!cfg || !A || !B || !C || !mean_ms || !first_ms || !aborted) {
+    gt::set_error("gt_measure: null argument");
+    return GT_EINVAL;
+  }
+  return gt::measure(*cfg, A, B, C, M, N, K, dtype, static_cast<hipStream_t>(stream), warmup, runs,
+                     abort_ms, mean_ms, first_ms, aborted);
+}
+
+int gt_reference_gemm(const void* A, const void* B, void* C, int64_t M, int64_t N, int64_t K,
+                      int dtype, void* stream) {
+  if (!A || !B || !C || M < 1 || N < 1 || K < 1 || (dtype != GT_F32 && dtype != GT_BF16)) {
+    gt::set_error("gt_reference_gemm: bad argument");
+    return GT_EINVAL;
+  }
+  if ((N + 63) / 64 > 2147483647 || (M + 3) / 4 > 65535) {
+    gt::set_error("gt_reference_gemm: shape exceeds the launch grid");
+    return GT_EINVAL;
+  }
+  hipError_t e = gt::launch_reference(A, B, static_cast<float*>(C), M, N, K, dtype,
+                                      static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) {
+    gt::set_error(std::string("reference launch: ") + hipGetErrorString(e));
+    return GT_EHIP;
+  }
+  return GT_OK;
+}
+
+int gt_compare(const void* C, const void* R, int64_t n, void* stream, double* rel) {
+  if (!C || !R || !rel || n < 1) {
+    gt::set_error("gt_compare: bad argument");
+    return GT_EINVAL;
+  }
+  return gt::compare_on_gpu(C, R, n, static_cast<hipStream_t>(stream), rel);
+}
+
+int gt_lower(const gt_config* cfg, int64_t M, int64_t N, int64_t K, int dtype,
+             gt_kernel_info* info) {
+  if (!cfg || !info) {
+    gt::set_error("gt_lower: null argument");
+    return GT_EINVAL;
+  }
+  // alignment-independent view: assume 16-byte aligned operands
+  gt::Lowered lw;
+  static const uint4 dummy[1] = {};
+  if (int rc = gt::lower(*cfg, M, N, K, dtype, dummy, dummy, nullptr, &lw)) return rc;
+  info->I = lw.L.I;
+  info->IK = lw.L.IK;
+  info->TM = static_cast<int32_t>(lw.L.TM);
+  info->TN = static_cast<int32_t>(lw.L.TN);
+  info->fast = lw.fast ? 1 : 0;
+  info->waves = static_cast<int32_t>(lw.L.W);
+  info->BM = lw.args.BM;
+  info->BN = lw.args.BN;
+  info->BK = lw.args.BK;
+  info->dbuf = lw.args.dbuf;
+  info->acc_regs = static_cast<int32_t>(lw.L.acc);
+  info->lds_bytes = static_cast<int32_t>(lw.lds);
+  info->grid_x = lw.grid.x;
+  info->grid_y = lw.grid.y;
+  return GT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,336 @@
+"""ctypes binding of libgemmtune (include/gemmtune.h), same names as the C ABI.
+
+Argument marshalling only: every step runs in the library. PyTorch supplies
+device memory (``tensor.data_ptr()``) and the stream
+(``torch.cuda.current_stream().cuda_stream``). Configurations are tuples
+``(m_levels, k_levels, n_levels, mfma)``, dimension order m, k, n.
+
+There is no fallback: if the library is not built, loading fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "_lib", "libgemmtune.so")
+MAXD = 4
+
+F32, BF16 = 0, 1
+ADJACENT, ANY_PAIR = 0, 1
+STATUS = {0: "ok", 1: "early-abort", 2: "launch-failure", 3: "mismatch"}
+STOP = {0: "budget", 1: "queue-empty", 2: "time-limit"}
+
+
+class GemmTuneError(RuntimeError):
+    pass
+
+
+class gt_space(ctypes.Structure):
+    _fields_ = [("M", ctypes.c_int64), ("N", ctypes.c_int64), ("K", ctypes.c_int64),
+                ("d_m", ctypes.c_int32), ("d_k", ctypes.c_int32), ("d_n", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("mfma_coord", ctypes.c_int32),
+                ("neighbour_mode", ctypes.c_int32)]
+
+
+class gt_config(ctypes.Structure):
+    _fields_ = [("d_m", ctypes.c_int32), ("d_k", ctypes.c_int32), ("d_n", ctypes.c_int32),
+                ("mfma", ctypes.c_int32),
+                ("m", ctypes.c_int64 * MAXD), ("k", ctypes.c_int64 * MAXD),
+                ("n", ctypes.c_int64 * MAXD),
+                ("legit", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+class gt_kernel_info(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("I", "IK", "TM", "TN", "fast", "waves", "BM", "BN", "BK", "dbuf", "acc_regs",
+                 "lds_bytes")] + [("grid_x", ctypes.c_int64), ("grid_y", ctypes.c_int64)]
+
+
+class gt_log_entry(ctypes.Structure):
+    _fields_ = [("rank", ctypes.c_uint64), ("cost_ms", ctypes.c_double),
+                ("first_ms", ctypes.c_double), ("rel_err", ctypes.c_double),
+                ("status", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+gt_cost_fn = ctypes.CFUNCTYPE(ctypes.c_double, ctypes.POINTER(gt_config), ctypes.c_uint64,
+                              ctypes.c_void_p)
+
+
+class gt_tune_opts(ctypes.Structure):
+    _fields_ = [("s0", ctypes.POINTER(gt_config)), ("rho", ctypes.c_int32),
+                ("runs", ctypes.c_int32), ("warmup", ctypes.c_int32), ("check", ctypes.c_int32),
+                ("budget", ctypes.c_int64), ("t_max_s", ctypes.c_double),
+                ("seed", ctypes.c_uint64), ("max_run_ms", ctypes.c_double),
+                ("abort_factor", ctypes.c_double),
+                ("A", ctypes.c_void_p), ("B", ctypes.c_void_p), ("C", ctypes.c_void_p),
+                ("c_ref", ctypes.c_void_p), ("stream", ctypes.c_void_p),
+                ("log", ctypes.POINTER(gt_log_entry)), ("log_cap", ctypes.c_int64)]
+
+
+class gt_tune_result(ctypes.Structure):
+    _fields_ = [("best", gt_config), ("best_rank", ctypes.c_uint64),
+                ("best_cost", ctypes.c_double), ("timed", ctypes.c_int64),
+                ("popped", ctypes.c_int64), ("skipped_illegit", ctypes.c_int64),
+                ("skipped_visited", ctypes.c_int64), ("failed", ctypes.c_int64),
+                ("wall_s", ctypes.c_double), ("stop_reason", ctypes.c_int32),
+                ("reserved", ctypes.c_int32)]
+
+
+EXPORTS = ("gt_space_size", "enumerate_configs", "config_rank", "config_unrank", "config_legit",
+           "neighbours", "gemm_run", "gt_measure", "gt_reference_gemm", "gt_compare",
+           "gt_lower", "gt_tune_opts_init", "tune_gbfs", "gt_last_error")
+
+_lib = None
+
+
+def lib():
+    """Load libgemmtune.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise GemmTuneError(f"{LIB_PATH} is missing: build it with "
+                            "`python -c 'import __graft_entry__ as g; g.build()'`")
+    L = ctypes.CDLL(LIB_PATH)
+    P, i64, u64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int
+    SP, CF = ctypes.POINTER(gt_space), ctypes.POINTER(gt_config)
+    L.gt_space_size.argtypes = [SP, ctypes.POINTER(u64)]
+    L.enumerate_configs.argtypes = [SP, u64, CF, u64, ctypes.POINTER(u64)]
+    L.config_rank.argtypes = [SP, CF, ctypes.POINTER(u64)]
+    L.config_unrank.argtypes = [SP, u64, CF]
+    L.config_legit.argtypes = [SP, CF, ctypes.POINTER(i32)]
+    L.neighbours.argtypes = [SP, CF, CF, i32, ctypes.POINTER(i32)]
+    L.gemm_run.argtypes = [CF, P, P, P, i64, i64, i64, i32, P]
+    L.gt_measure.argtypes = [CF, P, P, P, i64, i64, i64, i32, P, i32, i32, ctypes.c_double,
+                             ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double),
+                             ctypes.POINTER(i32)]
+    L.gt_reference_gemm.argtypes = [P, P, P, i64, i64, i64, i32, P]
+    L.gt_compare.argtypes = [P, P, i64, P, ctypes.POINTER(ctypes.c_double)]
+    L.gt_lower.argtypes = [CF, i64, i64, i64, i32, ctypes.POINTER(gt_kernel_info)]
+    L.gt_tune_opts_init.argtypes = [ctypes.POINTER(gt_tune_opts)]
+    L.tune_gbfs.argtypes = [SP, ctypes.POINTER(gt_tune_opts), gt_cost_fn, P,
+                            ctypes.POINTER(gt_tune_result)]
+    L.gt_last_error.restype = ctypes.c_char_p
+    for name in EXPORTS:
+        if name != "gt_last_error":
+            getattr(L, name).restype = ctypes.c_int
+    _lib = L
+    return L
+
+
+def _check(rc: int, what: str):
+    if rc != 0:
+        msg = lib().gt_last_error().decode(errors="replace")
+        raise GemmTuneError(f"{what} failed ({rc}): {msg}")
+
+
+def dtype_code(dtype) -> int:
+    if isinstance(dtype, int):
+        return dtype
+    s = str(dtype)
+    if s in ("f32", "torch.float32", "float32"):
+        return F32
+    if s in ("bf16", "torch.bfloat16", "bfloat16"):
+        return BF16
+    raise ValueError(f"unsupported dtype {dtype!r}")
+
+
+def to_c(cfg) -> gt_config:
+    c = gt_config()
+    m, k, n = cfg[0], cfg[1], cfg[2]
+    c.d_m, c.d_k, c.d_n = len(m), len(k), len(n)
+    for arr, vals in ((c.m, m), (c.k, k), (c.n, n)):
+        for i, v in enumerate(vals):
+            arr[i] = int(v)
+    c.mfma = int(cfg[3]) if len(cfg) > 3 else 0
+    return c
+
+
+def from_c(c: gt_config):
+    return (tuple(int(c.m[i]) for i in range(c.d_m)), tuple(int(c.k[i]) for i in range(c.d_k)),
+            tuple(int(c.n[i]) for i in range(c.d_n)), int(c.mfma))
+
+
+class Space:
+    """Configuration space ξ (§3.3 Eq.1–4) with the C-ABI's queries."""
+
+    def __init__(self, M, N, K, d=(4, 4, 4), dtype="f32", mfma_coord=False,
+                 mode=ADJACENT):
+        self.M, self.N, self.K = int(M), int(N), int(K)
+        self.d = tuple(int(x) for x in d)
+        self.dtype = dtype_code(dtype)
+        self.mfma_coord = bool(mfma_coord)
+        self.mode = int(mode)
+        s = gt_space()
+        s.M, s.N, s.K = self.M, self.N, self.K
+        s.d_m, s.d_k, s.d_n = self.d
+        s.dtype, s.mfma_coord, s.neighbour_mode = self.dtype, int(self.mfma_coord), self.mode
+        self.c = s
+
+    def size(self) -> int:
+        out = ctypes.c_uint64()
+        _check(lib().gt_space_size(ctypes.byref(self.c), ctypes.byref(out)), "gt_space_size")
+        return int(out.value)
+
+    def enumerate_raw(self, start: int, count: int):
+        buf = (gt_config * max(count, 1))()
+        n = ctypes.c_uint64()
+        _check(lib().enumerate_configs(ctypes.byref(self.c), start, buf, count, ctypes.byref(n)),
+               "enumerate_configs")
+        return buf, int(n.value)
+
+    def enumerate(self, start: int = 0, count: int | None = None):
+        if count is None:
+            count = self.size() - start
+        buf, n = self.enumerate_raw(start, count)
+        return [(from_c(buf[i]), bool(buf[i].legit)) for i in range(n)]
+
+    def rank(self, cfg) -> int:
+        out = ctypes.c_uint64()
+        _check(lib().config_rank(ctypes.byref(self.c), ctypes.byref(to_c(cfg)), ctypes.byref(out)),
+               "config_rank")
+        return int(out.value)
+
+    def unrank(self, r: int):
+        c = gt_config()
+        _check(lib().config_unrank(ctypes.byref(self.c), int(r), ctypes.byref(c)), "config_unrank")
+        return from_c(c)
+
+    def legit(self, cfg) -> bool:
+        J = ctypes.c_int()
+        _check(lib().config_legit(ctypes.byref(self.c), ctypes.byref(to_c(cfg)), ctypes.byref(J)),
+               "config_legit")
+        return bool(J.value)
+
+    def neighbours(self, cfg):
+        cap = 3 * MAXD * (MAXD - 1) + 1
+        out = (gt_config * cap)()
+        n = ctypes.c_int()
+        _check(lib().neighbours(ctypes.byref(self.c), ctypes.byref(to_c(cfg)), out, cap,
+                                ctypes.byref(n)), "neighbours")
+        return [(from_c(out[i]), bool(out[i].legit)) for i in range(n.value)]
+
+    def paper_s0(self):
+        """[D,1,…,1] per dimension (§5's start state), MFMA 16."""
+        return (tuple([self.M] + [1] * (self.d[0] - 1)), tuple([self.K] + [1] * (self.d[1] - 1)),
+                tuple([self.N] + [1] * (self.d[2] - 1)), 16 if self.mfma_coord else 0)
+
+
+def lower(cfg, M, N, K, dtype) -> dict:
+    info = gt_kernel_info()
+    _check(lib().gt_lower(ctypes.byref(to_c(cfg)), M, N, K, dtype_code(dtype), ctypes.byref(info)),
+           "gt_lower")
+    return {name: getattr(info, name) for name, _ in gt_kernel_info._fields_}
+
+
+# ---------------------------------------------------------------------------
+# GPU entry points (torch tensors for memory and stream)
+# ---------------------------------------------------------------------------
+
+def _stream(stream):
+    import torch
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _operands(A, B, C):
+    import torch
+    for t, name in ((A, "A"), (B, "B"), (C, "C")):
+        if not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous GPU tensor")
+    if A.dtype != B.dtype or A.dtype not in (torch.float32, torch.bfloat16):
+        raise ValueError("A and B must both be float32 or both bfloat16")
+    if C.dtype != torch.float32:
+        raise ValueError("C must be float32")
+    M, K = A.shape
+    K2, N = B.shape
+    if K2 != K or tuple(C.shape) != (M, N):
+        raise ValueError(f"shape mismatch A{tuple(A.shape)} B{tuple(B.shape)} C{tuple(C.shape)}")
+    return M, N, K, dtype_code(A.dtype)
+
+
+def gemm_run(cfg, A, B, C, stream=None):
+    M, N, K, dt = _operands(A, B, C)
+    _check(lib().gemm_run(ctypes.byref(to_c(cfg)), A.data_ptr(), B.data_ptr(), C.data_ptr(), M, N,
+                          K, dt, _stream(stream)), "gemm_run")
+    return C
+
+
+def gt_measure(cfg, A, B, C, warmup=1, runs=10, abort_ms=0.0, stream=None) -> dict:
+    M, N, K, dt = _operands(A, B, C)
+    mean, first, ab = ctypes.c_double(), ctypes.c_double(), ctypes.c_int()
+    _check(lib().gt_measure(ctypes.byref(to_c(cfg)), A.data_ptr(), B.data_ptr(), C.data_ptr(), M,
+                            N, K, dt, _stream(stream), warmup, runs, abort_ms, ctypes.byref(mean),
+                            ctypes.byref(first), ctypes.byref(ab)), "gt_measure")
+    return {"mean_ms": mean.value, "first_ms": first.value, "aborted": bool(ab.value)}
+
+
+def gt_reference_gemm(A, B, C, stream=None):
+    M, N, K, dt = _operands(A, B, C)
+    _check(lib().gt_reference_gemm(A.data_ptr(), B.data_ptr(), C.data_ptr(), M, N, K, dt,
+                                   _stream(stream)), "gt_reference_gemm")
+    return C
+
+
+def gt_compare(C, R, stream=None) -> float:
+    assert C.numel() == R.numel() and C.is_cuda and R.is_cuda
+    rel = ctypes.c_double()
+    _check(lib().gt_compare(C.data_ptr(), R.data_ptr(), C.numel(), _stream(stream),
+                            ctypes.byref(rel)), "gt_compare")
+    return rel.value
+
+
+def tune_gbfs(space: Space, budget: int, s0=None, rho: int = 5, seed: int = 0, runs: int = 10,
+              warmup: int = 1, check: bool = True, t_max_s: float = 0.0,
+              max_run_ms: float = 250.0, abort_factor: float = 50.0, A=None, B=None, C=None,
+              c_ref=None, cost_fn=None, stream=None) -> dict:
+    """Run G-BFS (Alg.1). With ``cost_fn(cfg, rank) -> float`` the costs are
+    synthetic (no GPU); otherwise A, B, C are GPU tensors and every candidate
+    is timed with ``gemm_run`` on the stream."""
+    L = lib()
+    o = gt_tune_opts()
+    _check(L.gt_tune_opts_init(ctypes.byref(o)), "gt_tune_opts_init")
+    s0c = to_c(s0) if s0 is not None else None
+    if s0c is not None:
+        o.s0 = ctypes.pointer(s0c)
+    o.rho, o.runs, o.warmup, o.check = rho, runs, warmup, int(check)
+    o.budget, o.t_max_s, o.seed = budget, t_max_s, seed
+    o.max_run_ms, o.abort_factor = max_run_ms, abort_factor
+    log = (gt_log_entry * budget)()
+    o.log = ctypes.cast(log, ctypes.POINTER(gt_log_entry))
+    o.log_cap = budget
+    cb = gt_cost_fn()  # NULL
+    keep = None
+    if cost_fn is not None:
+        def _cb(cptr, rank, _ctx):
+            return float(cost_fn(from_c(cptr.contents), int(rank)))
+        keep = cb = gt_cost_fn(_cb)
+    else:
+        M, N, K, dt = _operands(A, B, C)
+        if (M, N, K, dt) != (space.M, space.N, space.K, space.dtype):
+            raise ValueError("operands do not match the space")
+        o.A, o.B, o.C = A.data_ptr(), B.data_ptr(), C.data_ptr()
+        o.c_ref = c_ref.data_ptr() if c_ref is not None else None
+        o.stream = _stream(stream)
+    res = gt_tune_result()
+    _check(L.tune_gbfs(ctypes.byref(space.c), ctypes.byref(o), cb, None, ctypes.byref(res)),
+           "tune_gbfs")
+    del keep
+    n = int(res.timed)
+    entries = [{"rank": int(log[i].rank), "cost_ms": log[i].cost_ms, "first_ms": log[i].first_ms,
+                "rel_err": log[i].rel_err, "status": STATUS.get(log[i].status, str(log[i].status))}
+               for i in range(min(n, budget))]
+    return {"best": from_c(res.best), "best_rank": int(res.best_rank),
+            "best_cost": res.best_cost, "timed": n, "popped": int(res.popped),
+            "skipped_illegit": int(res.skipped_illegit),
+            "skipped_visited": int(res.skipped_visited), "failed": int(res.failed),
+            "wall_s": res.wall_s, "stop_reason": STOP.get(res.stop_reason, "?"),
+            "log": entries}
+
+
+def tflops(M, N, K, ms) -> float:
+    """2·M·N·K floating-point operations per run (one multiply-add = 2 flops)."""
+    return 2.0 * M * N * K / (ms * 1e-3) / 1e12 if ms > 0 and math.isfinite(ms) else 0.0

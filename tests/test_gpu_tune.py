@@ -1,0 +1,70 @@
+"""G-BFS on the GPU (through the C ABI).
+
+Timing noise means several trajectories are correct, so the checks are:
+the budget is respected, s* is the argmin of the timing log, no timed
+configuration mismatched the reference, the best configuration matches the
+fp64 oracle, and replaying the logged costs through the oracle's Alg.1
+reproduces the exact trajectory the GPU search took.
+"""
+import math
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+from workloads import make_inputs, raw_bytes
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def gt():
+    if not torch.cuda.is_available():
+        pytest.skip("needs a GPU")
+    from paper_1909_10616_amd import gemmtune
+    gemmtune.lib()
+    return gemmtune
+
+
+CASES = [
+    # (M, N, K, d, dtype, mfma_coord, budget, s0)
+    (256, 256, 256, (3, 3, 3), "f32", False, 64, None),
+    (512, 512, 512, (4, 4, 4), "bf16", True, 120, ((16, 1, 1, 32), (32, 1, 1, 16), (16, 1, 1, 32), 32)),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=["f32-256-paper-s0", "bf16-512-s0"])
+def test_gpu_search_is_consistent_and_replays_in_oracle(gt, orc, case):
+    M, N, K, d, dt, mc, budget, s0 = case
+    dev = torch.device("cuda:0")
+    A, B = make_inputs(M, N, K, dt, 0, "uniform" if dt == "f32" else "normal")
+    Ad, Bd = A.to(dev), B.to(dev)
+    C = torch.empty(M, N, device=dev)
+    sp = gt.Space(M, N, K, d, dt, mc)
+    print(f"tune {M}x{N}x{K} {dt} budget {budget}", flush=True)
+    res = gt.tune_gbfs(sp, budget=budget, s0=s0, rho=5, seed=3, A=Ad, B=Bd, C=C)
+    sys.stdout.flush()
+    log = res["log"]
+    assert res["timed"] == len(log) <= budget
+    assert res["timed"] == budget or res["stop_reason"] == "queue-empty"
+    assert all(e["status"] in ("ok", "early-abort") for e in log), \
+        [e for e in log if e["status"] not in ("ok", "early-abort")][:3]
+    costs = [e["cost_ms"] for e in log]
+    i = min(range(len(costs)), key=lambda t: (costs[t], t))
+    assert res["best_rank"] == log[i]["rank"] and res["best_cost"] == costs[i]
+    # the oracle's Alg.1 fed the logged costs takes the identical trajectory
+    os_ = orc.Space(M, N, K, d, dt, mc)
+    table = {e["rank"]: e["cost_ms"] for e in log}
+    start = s0 if s0 is not None else sp.paper_s0()
+    rep = orc.gbfs(os_, start, 5, budget, 3, lambda c, r: table.get(r, math.inf))
+    assert rep["log_ranks"] == [e["rank"] for e in log]
+    assert rep["best"] == res["best"]
+    # the best configuration's product matches the oracle
+    gt.gemm_run(res["best"], Ad, Bd, C)
+    torch.cuda.synchronize()
+    ref = orc.gemm(raw_bytes(A), raw_bytes(B), M, N, K, dt)
+    err = np.abs(C.cpu().numpy().astype(np.float64) - ref).max() / np.abs(ref).max()
+    assert err <= (1e-5 * K ** 0.5 if dt == "f32" else 2e-3)
+    print(f"best {res['best']} {gt.tflops(M, N, K, res['best_cost']):.2f} TFLOP/s after "
+          f"{res['timed']} timings in {res['wall_s']:.1f}s", flush=True)
