@@ -37,11 +37,15 @@ def _units():
         ("runtime", "runtime.cpp", []),
         ("aux_kernels", "aux_kernels.hip", []),
     ]
+    units.append(("gemm_lookup", "gemm_lookup.cpp", []))
     for dt, dn in ((0, "f32"), (1, "bf16")):
         for i in (16, 32):
-            for fast, pn in ((0, "generic"), (1, "fast")):
-                units.append((f"gemm_{dn}_{i}_{pn}", "gemm_inst.hip",
-                              [f"-DGT_DT={dt}", f"-DGT_I={i}", f"-DGT_FAST={fast}"]))
+            # CPR 0 is the generic path; the fast path needs CPR >= 64 / I
+            for cpr in (0, 2, 4, 8, 16):
+                if cpr and cpr < 64 // i:
+                    continue
+                units.append((f"gemm_{dn}_{i}_c{cpr}", "gemm_inst.hip",
+                              [f"-DGT_DT={dt}", f"-DGT_I={i}", f"-DGT_CPR={cpr}"]))
     return units
 
 

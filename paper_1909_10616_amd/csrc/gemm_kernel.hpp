@@ -45,6 +45,9 @@ struct KArgs {
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+// A 16-byte chunk as a native vector (HIP's u32x4 struct is copied by memcpy,
+// which keeps staging arrays out of registers).
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 template <int DT>
 struct Elem;
@@ -136,8 +139,8 @@ __device__ __forceinline__ void copy_tile(T* lds, const T* g, int64_t ld, int ro
     for (int e = tid; e < chunks; e += nthr) {
       const int r = e >> lgcpr;
       const int c = (e & ((1 << lgcpr) - 1)) << LGV;
-      *reinterpret_cast<uint4*>(lds + (r << lgcols) + c) =
-          *reinterpret_cast<const uint4*>(g + r * ld + c);
+      *reinterpret_cast<u32x4*>(lds + (r << lgcols) + c) =
+          *reinterpret_cast<const u32x4*>(g + r * ld + c);
     }
   } else {
     const int total = rows * cols;
@@ -195,7 +198,7 @@ __device__ void gemm_generic(const KArgs& a, char* smem) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = acc_t{};
 
-  auto load_stage = [&](int l, int buf) {
+  auto load_stage = [&](int l, int buf) __attribute__((always_inline)) {
     const int64_t kbase = (static_cast<int64_t>(l) * a.kSplit + z) * a.BK;
     T* as = As0 + buf * stage;
     T* bs = as + a.BM * a.BK;
@@ -203,7 +206,7 @@ __device__ void gemm_generic(const KArgs& a, char* smem) {
     copy_tile<T, Elem<DT>::VEC>(bs, Bg + kbase * a.N, a.N, a.BK, a.BN, a.lgBN, a.bVec, tid, nthr);
   };
 
-  auto compute = [&](int buf) {
+  auto compute = [&](int buf) __attribute__((always_inline)) {
     const T* as = As0 + buf * stage;
     const T* bs = as + a.BM * a.BK;
     const int nkk = (a.kBlk + IK - 1) / IK;
@@ -301,7 +304,7 @@ constexpr int kPfB = 1;  // B VEC×VEC blocks staged per thread
 
 // Transpose a VEC×VEC block held as VEC row chunks into VEC column chunks.
 template <int DT>
-__device__ __forceinline__ void transpose_block(const uint4* in, uint4* out) {
+__device__ __forceinline__ void transpose_block(const u32x4* in, u32x4* out) {
   if constexpr (DT == 1) {
     // 8×8 of 16-bit values; dword w of a chunk holds elements 2w (low), 2w+1 (high)
     const uint32_t* r = reinterpret_cast<const uint32_t*>(in);  // r[j*4 + w]
@@ -325,14 +328,26 @@ __device__ __forceinline__ void transpose_block(const uint4* in, uint4* out) {
   }
 }
 
-template <int DT, int I, int TM, int TN>
+template <int V>
+constexpr int ilog2c() {
+  return V <= 1 ? 0 : 1 + ilog2c<V / 2>();
+}
+
+// CPR = 16-byte chunks per LDS row = BK / VEC, a compile-time constant so
+// that the chunk-step loop unrolls: the fragments of chunk-step cs+1 are read
+// from LDS while the MFMAs of chunk-step cs run.
+template <int DT, int I, int TM, int TN, int CPR>
 __device__ void gemm_fast(const KArgs& a, char* smem) {
   using T = typename Elem<DT>::T;
   using acc_t = typename AccT<I>::type;
   constexpr int NACC = AccT<I>::N;
   constexpr int VEC = Elem<DT>::VEC;
   constexpr int LGV = VEC == 8 ? 3 : 2;
-  constexpr int G = 64 / I;
+  constexpr int G = 64 / I;          // lane groups of an MFMA operand
+  constexpr int NCS = CPR / G;       // chunk-steps per stage
+  constexpr int LGCPR = ilog2c<CPR>();
+  constexpr int NLINE = CPR >= 8 ? CPR / 8 : 1;  // 128-byte lines per LDS row
+  static_assert(NCS >= 1, "stage shallower than one MFMA K step");
   const int tid = threadIdx.x;
   const int nthr = blockDim.x;
   const int lane = tid & 63;
@@ -343,13 +358,11 @@ __device__ void gemm_fast(const KArgs& a, char* smem) {
   tile_of(a, gm, gn);
   const int z = blockIdx.y;
 
-  const int lgcpr = a.lgBK - LGV;  // chunks per row = BK / VEC
-  const int cpr = 1 << lgcpr;
-  const int achunks = a.BM << lgcpr;
-  const int nbk = a.BK >> LGV, nbn = a.BN >> LGV;  // B blocks along k and n
-  const int bblocks = nbk * nbn;
-  const int stage = achunks + (a.BN << lgcpr);  // chunks per stage
-  uint4* lds = reinterpret_cast<uint4*>(smem);
+  const int achunks = a.BM << LGCPR;
+  const int lgnbn = a.lgBN - LGV;    // B blocks along n = BN / VEC
+  const int bblocks = CPR << lgnbn;  // CPR blocks along k
+  const int stage = achunks + (a.BN << LGCPR);  // chunks per stage
+  u32x4* lds = reinterpret_cast<u32x4*>(smem);
 
   const T* Ag = reinterpret_cast<const T*>(a.A) + static_cast<int64_t>(gm) * a.BM * a.K;
   const T* Bg = reinterpret_cast<const T*>(a.B) + static_cast<int64_t>(gn) * a.BN;
@@ -358,49 +371,76 @@ __device__ void gemm_fast(const KArgs& a, char* smem) {
                          (bblocks + nthr * kPfB - 1) / (nthr * kPfB));
   const bool prefetch = rounds == 1;
 
-  uint4 ra[kPfA];
-  uint4 rb[kPfB * VEC];
-
-  auto gload = [&](int l, int round) {
-    const int64_t kbase = (static_cast<int64_t>(l) * a.kSplit + z) * a.BK;
+  // Stage-invariant global offsets and LDS slots of this thread's chunks.
+  // Every thread issues kPfA A-chunk and kPfB B-block loads with no branch
+  // (a load under a divergent branch is waited on at once): a thread whose
+  // chunk index lies past the tile takes the last chunk instead and later
+  // writes those same bytes to that chunk's own LDS slot.
+  int64_t aoff[kPfA];
+  int aslot[kPfA];
 #pragma unroll
-    for (int i = 0; i < kPfA; ++i) {
-      const int e = tid + (round * kPfA + i) * nthr;
-      if (e < achunks) {
-        const int r = e >> lgcpr, c = e & (cpr - 1);
-        ra[i] = *reinterpret_cast<const uint4*>(Ag + r * a.K + kbase + (c << LGV));
-      }
-    }
+  for (int i = 0; i < kPfA; ++i) {
+    const int e = min(tid + i * nthr, achunks - 1);
+    aoff[i] = static_cast<int64_t>(e >> LGCPR) * a.K + ((e & (CPR - 1)) << LGV);
+    aslot[i] = swz(e);
+  }
+  int64_t boff[kPfB];
+  int bq0[kPfB];
+#pragma unroll
+  for (int i = 0; i < kPfB; ++i) {
+    const int b = min(tid + i * nthr, bblocks - 1);
+    const int nb = b & ((1 << lgnbn) - 1), kb = b >> lgnbn;
+    boff[i] = static_cast<int64_t>(kb << LGV) * a.N + (nb << LGV);
+    bq0[i] = ((nb << LGV) << LGCPR) + kb;
+  }
+
+  u32x4 ra[kPfA];
+  u32x4 rb[kPfB * VEC];
+
+  auto gload = [&](int l) __attribute__((always_inline)) {
+    const int64_t kbase = (static_cast<int64_t>(l) * a.kSplit + z) * a.BK;
+    const T* ag = Ag + kbase;
+    const T* bg = Bg + kbase * a.N;
+#pragma unroll
+    for (int i = 0; i < kPfA; ++i) ra[i] = *reinterpret_cast<const u32x4*>(ag + aoff[i]);
+#pragma unroll
+    for (int i = 0; i < kPfB; ++i)
+#pragma unroll
+      for (int j = 0; j < VEC; ++j)
+        rb[i * VEC + j] = *reinterpret_cast<const u32x4*>(bg + boff[i] + j * a.N);
+  };
+
+  auto lstore = [&](int buf) __attribute__((always_inline)) {
+    u32x4* as = lds + buf * stage;
+    u32x4* bs = as + achunks;
+#pragma unroll
+    for (int i = 0; i < kPfA; ++i) as[aslot[i]] = ra[i];
 #pragma unroll
     for (int i = 0; i < kPfB; ++i) {
-      const int b = tid + (round * kPfB + i) * nthr;
-      if (b < bblocks) {
-        const int nb = b % nbn, kb = b / nbn;
-        const T* src = Bg + (kbase + (kb << LGV)) * a.N + (nb << LGV);
+      u32x4 t[VEC];
+      transpose_block<DT>(&rb[i * VEC], t);
 #pragma unroll
-        for (int j = 0; j < VEC; ++j) rb[i * VEC + j] = *reinterpret_cast<const uint4*>(src + j * a.N);
-      }
+      for (int j = 0; j < VEC; ++j) bs[swz(bq0[i] + (j << LGCPR))] = t[j];
     }
   };
 
-  auto lstore = [&](int buf, int round) {
-    uint4* as = lds + buf * stage;
-    uint4* bs = as + achunks;
+  // Tiles larger than the staging registers: load and store in rounds.
+  auto load_rounds = [&](int l, int buf) __attribute__((always_inline)) {
+    const int64_t kbase = (static_cast<int64_t>(l) * a.kSplit + z) * a.BK;
+    u32x4* as = lds + buf * stage;
+    u32x4* bs = as + achunks;
+    for (int e = tid; e < achunks; e += nthr)
+      as[swz(e)] = *reinterpret_cast<const u32x4*>(
+          Ag + static_cast<int64_t>(e >> LGCPR) * a.K + kbase + ((e & (CPR - 1)) << LGV));
+    for (int b = tid; b < bblocks; b += nthr) {
+      const int nb = b & ((1 << lgnbn) - 1), kb = b >> lgnbn;
+      const T* src = Bg + (kbase + (kb << LGV)) * a.N + (nb << LGV);
+      u32x4 r[VEC], t[VEC];
 #pragma unroll
-    for (int i = 0; i < kPfA; ++i) {
-      const int e = tid + (round * kPfA + i) * nthr;
-      if (e < achunks) as[swz(e)] = ra[i];
-    }
+      for (int j = 0; j < VEC; ++j) r[j] = *reinterpret_cast<const u32x4*>(src + j * a.N);
+      transpose_block<DT>(r, t);
 #pragma unroll
-    for (int i = 0; i < kPfB; ++i) {
-      const int b = tid + (round * kPfB + i) * nthr;
-      if (b < bblocks) {
-        const int nb = b % nbn, kb = b / nbn;
-        uint4 t[VEC];
-        transpose_block<DT>(&rb[i * VEC], t);
-#pragma unroll
-        for (int j = 0; j < VEC; ++j) bs[swz((((nb << LGV) + j) << lgcpr) + kb)] = t[j];
-      }
+      for (int j = 0; j < VEC; ++j) bs[swz((((nb << LGV) + j) << LGCPR) + kb)] = t[j];
     }
   };
 
@@ -410,68 +450,83 @@ __device__ void gemm_fast(const KArgs& a, char* smem) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = acc_t{};
 
-  const int arow0 = wm * a.WM + (lane % I);
-  const int bcol0 = wn * a.WN + (lane % I);
+  // Fragment addressing. Row r, chunk ch = cs·G + grp sits at slot
+  // swz(r·CPR + ch) = ((X_j ^ (cs·G & 7)) + (cs·G & ~7)) with
+  // X_j = swz(r·CPR + grp + 8j) − 8j for line j = (cs·G) / 8 of the row.
   const int grp = lane / I;
+  int xa[TM][NLINE], xb[TN][NLINE];
+#pragma unroll
+  for (int t = 0; t < TM; ++t)
+#pragma unroll
+    for (int j = 0; j < NLINE; ++j) {
+      const int q0 = ((wm * a.WM + t * I + (lane % I)) << LGCPR) + grp + 8 * j;
+      xa[t][j] = swz(q0) - 8 * j;
+    }
+#pragma unroll
+  for (int t = 0; t < TN; ++t)
+#pragma unroll
+    for (int j = 0; j < NLINE; ++j) {
+      const int q0 = ((wn * a.WN + t * I + (lane % I)) << LGCPR) + grp + 8 * j;
+      xb[t][j] = swz(q0) - 8 * j;
+    }
 
-  auto compute = [&](int buf) {
-    const uint4* as = lds + buf * stage;
-    const uint4* bs = as + achunks;
-    const int ncs = cpr / G;
-    for (int cs = 0; cs < ncs; ++cs) {
-      const int ch = cs * G + grp;
-      uint4 af[TM], bfv[TN];
+  u32x4 fa[2][TM], fb[2][TN];
+  auto load_frags = [&](const u32x4* as, int cs, int slot) __attribute__((always_inline)) {
+    const u32x4* bs = as + achunks;
+    const int c = cs * G;
+    const int j = CPR >= 8 ? (c >> 3) : 0;
 #pragma unroll
-      for (int t = 0; t < TM; ++t) af[t] = as[swz(((arow0 + t * I) << lgcpr) + ch)];
+    for (int t = 0; t < TM; ++t) fa[slot][t] = as[(xa[t][j] ^ (c & 7)) + (c & ~7)];
 #pragma unroll
-      for (int t = 0; t < TN; ++t) bfv[t] = bs[swz(((bcol0 + t * I) << lgcpr) + ch)];
-      if constexpr (DT == 1) {
+    for (int t = 0; t < TN; ++t) fb[slot][t] = bs[(xb[t][j] ^ (c & 7)) + (c & ~7)];
+  };
+  auto mfmas = [&](int slot) __attribute__((always_inline)) {
+    if constexpr (DT == 1) {
+#pragma unroll
+      for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+          acc[i][j] = mfma_bf16(__builtin_bit_cast(bf16x8, fa[slot][i]),
+                                __builtin_bit_cast(bf16x8, fb[slot][j]), acc[i][j]);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
 #pragma unroll
         for (int i = 0; i < TM; ++i)
 #pragma unroll
           for (int j = 0; j < TN; ++j)
-            acc[i][j] = mfma_bf16(__builtin_bit_cast(bf16x8, af[i]),
-                                  __builtin_bit_cast(bf16x8, bfv[j]), acc[i][j]);
-      } else {
-#pragma unroll
-        for (int q = 0; q < 4; ++q)
-#pragma unroll
-          for (int i = 0; i < TM; ++i)
-#pragma unroll
-            for (int j = 0; j < TN; ++j)
-              acc[i][j] = mfma_f32(__builtin_bit_cast(f32x4, af[i])[q],
-                                   __builtin_bit_cast(f32x4, bfv[j])[q], acc[i][j]);
-      }
+            acc[i][j] = mfma_f32(__builtin_bit_cast(f32x4, fa[slot][i])[q],
+                                 __builtin_bit_cast(f32x4, fb[slot][j])[q], acc[i][j]);
     }
   };
 
   if (prefetch) {
-    gload(0, 0);
-    lstore(0, 0);
+    gload(0);
+    lstore(0);
   } else {
-    for (int r = 0; r < rounds; ++r) {
-      gload(0, r);
-      lstore(0, r);
-    }
+    load_rounds(0, 0);
   }
   __syncthreads();
+  load_frags(lds, 0, 0);
   for (int l = 0; l < a.kLoop; ++l) {
     const int cur = a.dbuf ? (l & 1) : 0;
     const bool next = l + 1 < a.kLoop;
-    if (prefetch && next) gload(l + 1, 0);
-    compute(cur);
+    const u32x4* as = lds + cur * stage;
+    if (prefetch && next) gload(l + 1);
+#pragma unroll
+    for (int cs = 0; cs < NCS; ++cs) {
+      if (cs + 1 < NCS) load_frags(as, cs + 1, (cs + 1) & 1);
+      mfmas(cs & 1);
+    }
     if (next) {
       if (!a.dbuf) __syncthreads();
       const int nxt = a.dbuf ? (cur ^ 1) : 0;
-      if (prefetch) {
-        lstore(nxt, 0);
-      } else {
-        for (int r = 0; r < rounds; ++r) {
-          gload(l + 1, r);
-          lstore(nxt, r);
-        }
-      }
+      if (prefetch)
+        lstore(nxt);
+      else
+        load_rounds(l + 1, nxt);
       __syncthreads();
+      load_frags(lds + nxt * stage, 0, 0);
     }
   }
 
@@ -499,23 +554,27 @@ constexpr int max_waves() {
   return acc + 96 <= 128 ? 16 : (acc + 96 <= 256 ? 8 : 4);
 }
 
-template <int DT, int I, int TM, int TN, bool FAST>
-__global__ void __launch_bounds__(64 * (FAST ? (max_waves<I, TM, TN>() > 8 ? 8 : max_waves<I, TM, TN>())
-                                              : max_waves<I, TM, TN>()))
-    gemm_kernel(KArgs a) {
-  extern __shared__ uint4 gt_smem[];
+template <int I, int TM, int TN, int CPR>
+constexpr int launch_threads() {
+  return 64 * (CPR > 0 && max_waves<I, TM, TN>() > 8 ? 8 : max_waves<I, TM, TN>());
+}
+
+// CPR = 0: generic path; CPR > 0: fast path with BK = CPR·VEC.
+template <int DT, int I, int TM, int TN, int CPR>
+__global__ void __launch_bounds__((launch_threads<I, TM, TN, CPR>())) gemm_kernel(KArgs a) {
+  extern __shared__ u32x4 gt_smem[];
   char* smem = reinterpret_cast<char*>(gt_smem);
-  if constexpr (FAST)
-    gemm_fast<DT, I, TM, TN>(a, smem);
+  if constexpr (CPR > 0)
+    gemm_fast<DT, I, TM, TN, CPR>(a, smem);
   else
     gemm_generic<DT, I, TM, TN>(a, smem);
 }
 
 using LaunchFn = hipError_t (*)(const KArgs&, dim3, dim3, size_t, hipStream_t);
 
-template <int DT, int I, int TM, int TN, bool FAST>
+template <int DT, int I, int TM, int TN, int CPR>
 hipError_t launch_gemm(const KArgs& a, dim3 grid, dim3 block, size_t lds, hipStream_t s) {
-  auto fn = gemm_kernel<DT, I, TM, TN, FAST>;
+  auto fn = gemm_kernel<DT, I, TM, TN, CPR>;
   static bool attr_set = false;  // raise the dynamic LDS limit once per kernel
   if (!attr_set) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
@@ -537,15 +596,11 @@ hipError_t launch_gemm(const KArgs& a, dim3 grid, dim3 block, size_t lds, hipStr
   X(1, 32) X(2, 16) X(4, 8) X(8, 4) X(16, 2) X(32, 1) X(1, 64) X(2, 32) X(4, 16) X(8, 8)     \
       X(16, 4) X(32, 2) X(64, 1)
 
-// Lookup of one translation unit: (TM, TN) → launcher, or nullptr.
-using LookupFn = LaunchFn (*)(int, int);
-LaunchFn lookup_f32_16_generic(int, int);
-LaunchFn lookup_f32_32_generic(int, int);
-LaunchFn lookup_bf16_16_generic(int, int);
-LaunchFn lookup_bf16_32_generic(int, int);
-LaunchFn lookup_f32_16_fast(int, int);
-LaunchFn lookup_f32_32_fast(int, int);
-LaunchFn lookup_bf16_16_fast(int, int);
-LaunchFn lookup_bf16_32_fast(int, int);
+// Chunks per LDS row with a fast-path instantiation (BK = CPR·VEC).
+constexpr int kFastCpr[] = {2, 4, 8, 16};
+
+// Kernel of (dtype, I, CPR, TM, TN), CPR = 0 for the generic path; nullptr
+// when not instantiated.
+LaunchFn find_gemm_kernel(int dtype, int I, int cpr, int TM, int TN);
 
 }  // namespace gt

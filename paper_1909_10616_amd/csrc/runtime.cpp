@@ -27,15 +27,6 @@ int ilog2(int64_t v) {
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-LaunchFn find_kernel(int dtype, int I, bool fast, int TM, int TN) {
-  if (dtype == GT_F32) {
-    if (I == 16) return fast ? lookup_f32_16_fast(TM, TN) : lookup_f32_16_generic(TM, TN);
-    return fast ? lookup_f32_32_fast(TM, TN) : lookup_f32_32_generic(TM, TN);
-  }
-  if (I == 16) return fast ? lookup_bf16_16_fast(TM, TN) : lookup_bf16_16_generic(TM, TN);
-  return fast ? lookup_bf16_32_fast(TM, TN) : lookup_bf16_32_generic(TM, TN);
-}
-
 int hip_fail(hipError_t e, const char* what) {
   set_error(std::string(what) + ": " + hipGetErrorString(e));
   return GT_EHIP;
@@ -69,9 +60,11 @@ int lower(const gt_config& c, int64_t M, int64_t N, int64_t K, int dtype, const 
   levels_of(c, dtype, &L);
   const int vec = dtype == GT_BF16 ? 8 : 4;
   const int G = 64 / L.I;
+  const int64_t cpr = L.BK / vec;  // 16-byte chunks per LDS row
+  const bool cpr_ok = L.BK % vec == 0 && (cpr == 2 || cpr == 4 || cpr == 8 || cpr == 16);
   const bool fast = L.blkM % L.I == 0 && L.blkN % L.I == 0 && L.kBlk % L.IK == 0 &&
-                    L.BK % (vec * G) == 0 && L.BN % vec == 0 && K % vec == 0 && N % vec == 0 &&
-                    L.W <= 8 && aligned16(A) && aligned16(B);
+                    L.BK % (vec * G) == 0 && cpr_ok && L.BN % vec == 0 && K % vec == 0 &&
+                    N % vec == 0 && L.W <= 8 && aligned16(A) && aligned16(B);
   const int64_t stage_bytes = (L.BM * L.BK + L.BK * L.BN) * L.elem;
   const bool dbuf = L.kLoop >= 2 && 2 * stage_bytes <= kLdsMax;
 
@@ -112,7 +105,8 @@ int lower(const gt_config& c, int64_t M, int64_t N, int64_t K, int dtype, const 
   out->block = dim3(static_cast<unsigned>(64 * L.W), 1, 1);
   out->lds = static_cast<size_t>(stage_bytes * (dbuf ? 2 : 1));
   out->fast = fast;
-  out->fn = find_kernel(dtype, L.I, fast, static_cast<int>(L.TM), static_cast<int>(L.TN));
+  out->fn = find_gemm_kernel(dtype, L.I, fast ? static_cast<int>(cpr) : 0,
+                             static_cast<int>(L.TM), static_cast<int>(L.TN));
   if (!out->fn) {
     set_error("no kernel instantiation for this MFMA tile shape");
     return GT_ENOKERNEL;

@@ -160,7 +160,7 @@ int tune_gbfs(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn cost, void* 
       int rc = gt_reference_gemm(o->A, o->B, g.c_ref, sp->M, sp->N, sp->K, sp->dtype, o->stream);
       if (rc == GT_OK && hipStreamSynchronize(g.s) != hipSuccess) rc = GT_EHIP;
       if (rc != GT_OK) {
-        if (owned_ref) hipFree(owned_ref);
+        if (owned_ref) (void)hipFree(owned_ref);
         return rc;
       }
     }
@@ -250,7 +250,7 @@ int tune_gbfs(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn cost, void* 
   out->best_rank = best;
   out->best_cost = cost_min;
   out->wall_s = elapsed();
-  if (owned_ref) hipFree(owned_ref);
+  if (owned_ref) (void)hipFree(owned_ref);
   return GT_OK;
 }
 
