@@ -138,6 +138,8 @@ typedef struct gt_kernel_info {
   int32_t I, IK;             /* MFMA instruction size and its K */
   int32_t TM, TN;            /* MFMA tiles per wavefront */
   int32_t fast;              /* 1: vectorised swizzled-LDS path */
+  int32_t dl;                /* 1: fast path with direct global->LDS loads */
+  int32_t ring;              /* LDS ring stages of the direct-load path */
   int32_t waves;             /* wavefronts per workgroup */
   int32_t BM, BN, BK;        /* workgroup tile and LDS stage depth */
   int32_t dbuf;              /* LDS double buffering */

@@ -20,6 +20,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
+#include <type_traits>
 
 namespace gt {
 
@@ -40,6 +41,8 @@ struct KArgs {
   int32_t atomic;          // split-K: accumulate with fp32 atomics
   int32_t remap;           // XCD-aware workgroup order
   int32_t aVec, bVec;      // generic path: 1 or 16-byte vector tile loads
+  int32_t dl;              // fast path: direct global->LDS loads into a ring
+  int32_t ns;              // ring stages (direct-load path)
 };
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -371,19 +374,18 @@ __device__ void gemm_fast(const KArgs& a, char* smem) {
                          (bblocks + nthr * kPfB - 1) / (nthr * kPfB));
   const bool prefetch = rounds == 1;
 
-  // Stage-invariant global offsets and LDS slots of this thread's chunks.
-  // Every thread issues kPfA A-chunk and kPfB B-block loads with no branch
-  // (a load under a divergent branch is waited on at once): a thread whose
-  // chunk index lies past the tile takes the last chunk instead and later
-  // writes those same bytes to that chunk's own LDS slot.
-  int64_t aoff[kPfA];
-  int aslot[kPfA];
-#pragma unroll
-  for (int i = 0; i < kPfA; ++i) {
-    const int e = min(tid + i * nthr, achunks - 1);
-    aoff[i] = static_cast<int64_t>(e >> LGCPR) * a.K + ((e & (CPR - 1)) << LGV);
-    aslot[i] = swz(e);
-  }
+  // This thread's chunks: A chunk i is e_i = ta + i·nthr with ta = tid, i.e.
+  // row (ta >> LGCPR) + i·(nthr >> LGCPR), column chunk ta & (CPR − 1), so
+  // one base offset and a uniform row stride address all of them. Tile and
+  // thread counts are powers of two: either every thread owns na chunks, or
+  // the tile has fewer chunks than threads, na = 1 and the surplus threads
+  // take the last chunk (ta clamped) and later write those same bytes to
+  // its slot. The loads therefore sit under wavefront-uniform conditions only.
+  const int na = __builtin_amdgcn_readfirstlane(min(kPfA, (achunks + nthr - 1) / nthr));
+  const int nbb = __builtin_amdgcn_readfirstlane(min(kPfB, (bblocks + nthr - 1) / nthr));
+  const int ta = min(tid, achunks - 1);
+  const int64_t aoff0 = static_cast<int64_t>(ta >> LGCPR) * a.K + ((ta & (CPR - 1)) << LGV);
+  const int64_t astride = static_cast<int64_t>(nthr >> LGCPR) * a.K;
   int64_t boff[kPfB];
   int bq0[kPfB];
 #pragma unroll
@@ -399,29 +401,34 @@ __device__ void gemm_fast(const KArgs& a, char* smem) {
 
   auto gload = [&](int l) __attribute__((always_inline)) {
     const int64_t kbase = (static_cast<int64_t>(l) * a.kSplit + z) * a.BK;
-    const T* ag = Ag + kbase;
+    const T* ag = Ag + kbase + aoff0;
     const T* bg = Bg + kbase * a.N;
 #pragma unroll
-    for (int i = 0; i < kPfA; ++i) ra[i] = *reinterpret_cast<const u32x4*>(ag + aoff[i]);
+    for (int i = 0; i < kPfA; ++i)
+      if (i < na) ra[i] = *reinterpret_cast<const u32x4*>(ag + i * astride);
 #pragma unroll
     for (int i = 0; i < kPfB; ++i)
+      if (i < nbb) {
 #pragma unroll
-      for (int j = 0; j < VEC; ++j)
-        rb[i * VEC + j] = *reinterpret_cast<const u32x4*>(bg + boff[i] + j * a.N);
+        for (int j = 0; j < VEC; ++j)
+          rb[i * VEC + j] = *reinterpret_cast<const u32x4*>(bg + boff[i] + j * a.N);
+      }
   };
 
   auto lstore = [&](int buf) __attribute__((always_inline)) {
     u32x4* as = lds + buf * stage;
     u32x4* bs = as + achunks;
 #pragma unroll
-    for (int i = 0; i < kPfA; ++i) as[aslot[i]] = ra[i];
+    for (int i = 0; i < kPfA; ++i)
+      if (i < na) as[swz(ta + i * nthr)] = ra[i];
 #pragma unroll
-    for (int i = 0; i < kPfB; ++i) {
-      u32x4 t[VEC];
-      transpose_block<DT>(&rb[i * VEC], t);
+    for (int i = 0; i < kPfB; ++i)
+      if (i < nbb) {
+        u32x4 t[VEC];
+        transpose_block<DT>(&rb[i * VEC], t);
 #pragma unroll
-      for (int j = 0; j < VEC; ++j) bs[swz(bq0[i] + (j << LGCPR))] = t[j];
-    }
+        for (int j = 0; j < VEC; ++j) bs[swz(bq0[i] + (j << LGCPR))] = t[j];
+      }
   };
 
   // Tiles larger than the staging registers: load and store in rounds.
@@ -500,37 +507,296 @@ __device__ void gemm_fast(const KArgs& a, char* smem) {
     }
   };
 
-  if (prefetch) {
-    gload(0);
-    lstore(0);
-  } else {
-    load_rounds(0, 0);
-  }
-  __syncthreads();
-  load_frags(lds, 0, 0);
-  for (int l = 0; l < a.kLoop; ++l) {
-    const int cur = a.dbuf ? (l & 1) : 0;
-    const bool next = l + 1 < a.kLoop;
-    const u32x4* as = lds + cur * stage;
-    if (prefetch && next) gload(l + 1);
+  auto compute = [&](const u32x4* as) __attribute__((always_inline)) {
 #pragma unroll
     for (int cs = 0; cs < NCS; ++cs) {
       if (cs + 1 < NCS) load_frags(as, cs + 1, (cs + 1) & 1);
       mfmas(cs & 1);
     }
-    if (next) {
-      if (!a.dbuf) __syncthreads();
-      const int nxt = a.dbuf ? (cur ^ 1) : 0;
-      if (prefetch)
-        lstore(nxt);
-      else
-        load_rounds(l + 1, nxt);
+  };
+
+  // Main loop: every stage but the last is one straight-line block — the
+  // next stage's global loads, this stage's LDS fragments and MFMAs, the
+  // next stage's LDS stores — so the scheduler can interleave them.
+  auto main_loop = [&](auto dbuf_tag) __attribute__((always_inline)) {
+    constexpr bool DB = decltype(dbuf_tag)::value;
+    gload(0);
+    lstore(0);
+    __syncthreads();
+    load_frags(lds, 0, 0);
+    int l = 0;
+    for (; l + 1 < a.kLoop; ++l) {
+      const int cur = DB ? (l & 1) : 0;
+      const int nxt = DB ? (cur ^ 1) : 0;
+      gload(l + 1);
+      // keep the next stage's loads ahead of this stage's MFMAs
+      __builtin_amdgcn_sched_barrier(0);
+      compute(lds + cur * stage);
+      if constexpr (!DB) __syncthreads();
+      lstore(nxt);
       __syncthreads();
       load_frags(lds + nxt * stage, 0, 0);
+    }
+    compute(lds + (DB ? (l & 1) : 0) * stage);
+  };
+
+  if (prefetch) {
+    if (a.dbuf)
+      main_loop(std::true_type{});
+    else
+      main_loop(std::false_type{});
+  } else {
+    load_rounds(0, 0);
+    __syncthreads();
+    load_frags(lds, 0, 0);
+    for (int l = 0; l < a.kLoop; ++l) {
+      const int cur = a.dbuf ? (l & 1) : 0;
+      compute(lds + cur * stage);
+      if (l + 1 < a.kLoop) {
+        if (!a.dbuf) __syncthreads();
+        const int nxt = a.dbuf ? (cur ^ 1) : 0;
+        load_rounds(l + 1, nxt);
+        __syncthreads();
+        load_frags(lds + nxt * stage, 0, 0);
+      }
     }
   }
 
   float* Cw = a.C + static_cast<int64_t>(gm) * a.BM * a.N + static_cast<int64_t>(gn) * a.BN;
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+#pragma unroll
+      for (int e = 0; e < NACC; ++e) {
+        const int r = wm * a.WM + i * I + out_row<I>(lane, e);
+        const int c = wn * a.WN + j * I + (lane % I);
+        put(a.atomic != 0, Cw + static_cast<int64_t>(r) * a.N + c, acc[i][j][e]);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Fast path with direct global→LDS loads (bf16)
+// ---------------------------------------------------------------------------
+//
+// Each global_load_lds_dwordx4 of a wavefront writes 64 consecutive 16-byte
+// LDS slots (lane j → slot base + j) from 64 per-lane global addresses, so
+// tiles reach LDS without passing through registers and a ring of ns stages
+// keeps ns − 1 stages of loads in flight. A sits in LDS as [m][k] chunks,
+// XOR-swizzled by swz(); B stays [k][n] with the chunks of row k XOR-ed by
+// bswz(k), and its MFMA operands are read with the transposing LDS read: inside a
+// 16-lane group, lane l receives element (l & 3) of the 8 bytes addressed by
+// lane 4j + (l >> 2) as its j-th value, so lanes addressing rows k0 + (i >> 2),
+// columns n0 + 4(i & 3) hand lane l four consecutive k of column n0 + l.
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+constexpr int kMaxDlInst = 16;
+
+// XOR applied to the 16-byte chunk index of B row k in LDS. A transposing
+// read touches rows k0 … k0+3 (k0 ≡ 0 mod 4) and, per 16-lane group, two
+// adjacent chunks (four per 32 lanes); f(k mod 4) ∈ {0, 6, 10, 12} sends those
+// to 8 distinct 16-byte bank slots mod 128 B and 16 distinct mod 256 B.
+__device__ __forceinline__ int bswz(int k, int cprb) {
+  const int j = k & 3;
+  return ((j << 2) | (((j ^ (j >> 1)) & 1) << 1)) & (cprb - 1);
+}  // direct-load instructions per wavefront per stage
+
+// vmcnt field of s_waitcnt on gfx9: bits [3:0] and [15:14]; lgkmcnt [11:8], expcnt [6:4].
+template <int N>
+__device__ __forceinline__ void waitcnt_vm() {
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xf << 8));
+}
+
+__device__ __forceinline__ void waitcnt_lgkm0() {
+  __builtin_amdgcn_s_waitcnt(0xf | (0x3 << 14) | (0x7 << 4));  // lgkmcnt(0) only
+}
+
+__device__ __forceinline__ void wait_vm_at_most(int n) {
+  if (n >= 48) waitcnt_vm<48>();
+  else if (n >= 32) waitcnt_vm<32>();
+  else if (n >= 24) waitcnt_vm<24>();
+  else if (n >= 16) waitcnt_vm<16>();
+  else if (n >= 12) waitcnt_vm<12>();
+  else if (n >= 8) waitcnt_vm<8>();
+  else if (n >= 6) waitcnt_vm<6>();
+  else if (n >= 4) waitcnt_vm<4>();
+  else if (n >= 3) waitcnt_vm<3>();
+  else if (n >= 2) waitcnt_vm<2>();
+  else if (n >= 1) waitcnt_vm<1>();
+  else waitcnt_vm<0>();
+}
+
+// One 16-byte-per-lane direct global→LDS load (lane j → LDS byte address
+// lds_base + 16·j). Written as inline assembly so that the compiler does not
+// see an LDS write it would have to wait for before every LDS read (it cannot
+// tell the ring slots apart); the ring's vmcnt accounting is done explicitly.
+__device__ __forceinline__ void dma_load16(const void* src, uint32_t lds_base) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(lds_base)
+               : "memory", "m0");
+}
+
+// Byte offset inside LDS of a pointer into the kernel's dynamic LDS.
+__device__ __forceinline__ uint32_t lds_off(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>(
+      (const __attribute__((address_space(3))) char*)(p)));
+}
+
+template <int I, int TM, int TN, int CPR>
+__device__ void gemm_fast_dl(const KArgs& a, char* smem) {
+  using T = uint16_t;
+  using acc_t = typename AccT<I>::type;
+  constexpr int NACC = AccT<I>::N;
+  constexpr int G = 64 / I;
+  constexpr int NCS = CPR / G;
+  constexpr int LGCPR = ilog2c<CPR>();
+  constexpr int NLINE = CPR >= 8 ? CPR / 8 : 1;
+  static_assert(NCS >= 1, "stage shallower than one MFMA K step");
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int nw = blockDim.x >> 6;
+  const int wm = wave % a.wavesM;
+  const int wn = wave / a.wavesM;
+  int gm, gn;
+  tile_of(a, gm, gn);
+  const int z = blockIdx.y;
+
+  const int BM = a.BM, BN = a.BN, BK = a.BK;
+  const int cprb = BN >> 3;                 // 16-byte chunks per B row
+  const int achunks = BM << LGCPR;
+  const int bchunks = BK * cprb;
+  const int stage = achunks + bchunks;      // 16-byte slots per stage
+  const int pa = achunks >> 6, pb = bchunks >> 6;
+  const int ninst = (pa + pb) / nw;         // load instructions per wavefront per stage
+  const int ns = a.ns;
+  u32x4* lds = reinterpret_cast<u32x4*>(smem);
+  const T* Ag = reinterpret_cast<const T*>(a.A) + static_cast<int64_t>(gm) * BM * a.K;
+  const T* Bg = reinterpret_cast<const T*>(a.B) + static_cast<int64_t>(gn) * BN;
+
+  // Load instruction p of a stage fills slots p·64 … p·64+63; wavefront w
+  // issues p = w, w + nw, … (A instructions first, then B). Each lane works
+  // out the chunk its slot holds: A slot s holds chunk swz(s) (swz is an
+  // involution), B slot (k, cs) holds row k, chunk cs ^ bswz(k).
+  const int lgcprb = a.lgBN - 3;
+  const int na_w = pa / nw, nb_w = pb / nw;
+  auto issue = [&](int l, int slot) __attribute__((always_inline)) {
+    const int64_t kbase = (static_cast<int64_t>(l) * a.kSplit + z) * BK;
+    const T* ag = Ag + kbase;
+    const T* bg = Bg + kbase * a.N;
+    u32x4* base = lds + slot * stage;
+    for (int t = 0; t < na_w; ++t) {
+      const int p = wave + t * nw;
+      const int q = swz((p << 6) + lane);
+      const T* src = ag + (q >> LGCPR) * a.K + ((q & (CPR - 1)) << 3);
+      dma_load16(src, __builtin_amdgcn_readfirstlane(lds_off(base + (p << 6))));
+    }
+    u32x4* bbase = base + achunks;
+    for (int t = 0; t < nb_w; ++t) {
+      const int p = wave + t * nw;
+      const int sidx = (p << 6) + lane;
+      const int k = sidx >> lgcprb, cs = sidx & (cprb - 1);
+      const T* src = bg + k * a.N + ((cs ^ bswz(k, cprb)) << 3);
+      dma_load16(src, __builtin_amdgcn_readfirstlane(lds_off(bbase + (p << 6))));
+    }
+  };
+
+  acc_t acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j) acc[i][j] = acc_t{};
+
+  // A fragment slots as in the register-staged path.
+  const int grp = lane / I;
+  int xa[TM][NLINE];
+#pragma unroll
+  for (int t = 0; t < TM; ++t)
+#pragma unroll
+    for (int j = 0; j < NLINE; ++j) {
+      const int q0 = ((wm * a.WM + t * I + (lane % I)) << LGCPR) + grp + 8 * j;
+      xa[t][j] = swz(q0) - 8 * j;
+    }
+  // B operand addressing: in 16-lane group g16, input lane i covers row
+  // k0 + (i >> 2) (+4 for the second read), columns n0 + 4(i & 3).
+  const int i16 = lane & 15, g16 = lane >> 4;
+  const int kgrp = I == 32 ? (g16 >> 1) : g16;           // which 8-k group of the step
+  const int ncol0 = (I == 32 ? 16 * (g16 & 1) : 0) + 4 * (i16 & 3);
+  int bcol[TN];
+#pragma unroll
+  for (int t = 0; t < TN; ++t) bcol[t] = wn * a.WN + t * I + ncol0;  // column of this lane's 4 values
+  const int krow_l = kgrp * 8 + (i16 >> 2);
+
+  u32x4 fa[2][TM];
+  u32x4 fb[2][TN];
+  auto load_frags = [&](const u32x4* as, int cs, int fs) __attribute__((always_inline)) {
+    const int c = cs * G;
+    const int j = CPR >= 8 ? (c >> 3) : 0;
+#pragma unroll
+    for (int t = 0; t < TM; ++t) fa[fs][t] = as[(xa[t][j] ^ (c & 7)) + (c & ~7)];
+    const char* bs = reinterpret_cast<const char*>(as + achunks);
+#pragma unroll
+    for (int t = 0; t < TN; ++t) {
+      s16x4 h[2];
+#pragma unroll
+      for (int hh = 0; hh < 2; ++hh) {
+        const int k = cs * (G * 8) + krow_l + 4 * hh;
+        const int col = bcol[t];
+        const int chunk = (col >> 3) ^ bswz(k, cprb);
+        const char* addr = bs + (k * cprb + chunk) * 16 + (col & 4) * 2;
+        h[hh] = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4*)(addr));
+      }
+      fb[fs][t] = __builtin_bit_cast(u32x4, __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7));
+    }
+  };
+  auto mfmas = [&](int fs) __attribute__((always_inline)) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = mfma_bf16(__builtin_bit_cast(bf16x8, fa[fs][i]),
+                              __builtin_bit_cast(bf16x8, fb[fs][j]), acc[i][j]);
+  };
+
+  // Ring schedule: stages 0 … ns−1 are issued up front; at the boundary after
+  // stage l's last LDS reads, stage l + ns is issued into stage l's slot. The
+  // boundary (wait for stage l + 1, barrier, issue, first fragments of stage
+  // l + 1) sits in front of stage l's last chunk-step of MFMAs, which then
+  // overlap it.
+  for (int l = 0; l < ns && l < a.kLoop; ++l) issue(l, l);
+  wait_vm_at_most(__builtin_amdgcn_readfirstlane(min(ns - 1, a.kLoop - 1) * ninst));
+  __builtin_amdgcn_s_barrier();
+  load_frags(lds, 0, 0);
+  for (int l = 0; l < a.kLoop; ++l) {
+    const int cur = l % ns;
+    const u32x4* as = lds + cur * stage;
+#pragma unroll
+    for (int cs = 0; cs + 1 < NCS; ++cs) {
+      load_frags(as, cs + 1, (cs + 1) & 1);
+      mfmas(cs & 1);
+    }
+    const bool more = l + 1 < a.kLoop;
+    const u32x4* nx = lds + ((l + 1) % ns) * stage;
+    if (more) {
+      // stages issued after stage l + 1: l + 2 … min(l + ns − 1, kLoop − 1)
+      wait_vm_at_most(__builtin_amdgcn_readfirstlane(min(ns - 2, a.kLoop - 2 - l) * ninst));
+      waitcnt_lgkm0();  // this wavefront's reads of slot cur are complete
+      // every wavefront: stage l + 1 landed, done reading slot cur
+      __builtin_amdgcn_s_barrier();
+      if (l + ns < a.kLoop) issue(l + ns, cur);
+      if constexpr (NCS >= 2) load_frags(nx, 0, 0);  // the last chunk-step uses slot 1
+    }
+    mfmas((NCS - 1) & 1);
+    if constexpr (NCS == 1) {
+      if (more) load_frags(nx, 0, 0);
+    }
+  }
+
+  float* Cw = a.C + static_cast<int64_t>(gm) * BM * a.N + static_cast<int64_t>(gn) * BN;
 #pragma unroll
   for (int i = 0; i < TM; ++i) {
 #pragma unroll
@@ -564,7 +830,12 @@ template <int DT, int I, int TM, int TN, int CPR>
 __global__ void __launch_bounds__((launch_threads<I, TM, TN, CPR>())) gemm_kernel(KArgs a) {
   extern __shared__ u32x4 gt_smem[];
   char* smem = reinterpret_cast<char*>(gt_smem);
-  if constexpr (CPR > 0)
+  if constexpr (CPR > 0 && DT == 1) {
+    if (a.dl)
+      gemm_fast_dl<I, TM, TN, CPR>(a, smem);
+    else
+      gemm_fast<DT, I, TM, TN, CPR>(a, smem);
+  } else if constexpr (CPR > 0)
     gemm_fast<DT, I, TM, TN, CPR>(a, smem);
   else
     gemm_generic<DT, I, TM, TN>(a, smem);

@@ -4,6 +4,7 @@
 // helpers.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -67,6 +68,15 @@ int lower(const gt_config& c, int64_t M, int64_t N, int64_t K, int dtype, const 
                     N % vec == 0 && L.W <= 8 && aligned16(A) && aligned16(B);
   const int64_t stage_bytes = (L.BM * L.BK + L.BK * L.BN) * L.elem;
   const bool dbuf = L.kLoop >= 2 && 2 * stage_bytes <= kLdsMax;
+  // bf16 fast path with direct global->LDS loads into a ring of ns stages:
+  // whole 64-slot load instructions, an even split over the wavefronts, at
+  // most 16 instructions per wavefront and stage, 32-bit element offsets
+  const int64_t achunks = L.BM * L.BK / 8, bchunks = L.BK * L.BN / 8;
+  const int64_t dl_inst = (achunks + bchunks) / 64;
+  const int64_t ns = std::min<int64_t>(8, kLdsMax / std::max<int64_t>(stage_bytes, 1));
+  const bool dl = fast && dtype == GT_BF16 && achunks % (64 * L.W) == 0 &&
+                  bchunks % (64 * L.W) == 0 && dl_inst / L.W <= 16 && ns >= 2 &&
+                  L.BM * K < (int64_t{1} << 31) && L.BK * N < (int64_t{1} << 31);
 
   KArgs& a = out->args;
   std::memset(&a, 0, sizeof(a));
@@ -100,10 +110,12 @@ int lower(const gt_config& c, int64_t M, int64_t N, int64_t K, int dtype, const 
   a.remap = (L.gridM * L.gridN) % 8 == 0 ? 1 : 0;
   a.aVec = (L.BK % vec == 0 && K % vec == 0 && aligned16(A)) ? vec : 1;
   a.bVec = (L.BN % vec == 0 && N % vec == 0 && aligned16(B)) ? vec : 1;
+  a.dl = dl ? 1 : 0;
+  a.ns = dl ? static_cast<int32_t>(ns) : 0;
 
   out->grid = dim3(static_cast<unsigned>(L.gridM * L.gridN), static_cast<unsigned>(L.kSplit), 1);
   out->block = dim3(static_cast<unsigned>(64 * L.W), 1, 1);
-  out->lds = static_cast<size_t>(stage_bytes * (dbuf ? 2 : 1));
+  out->lds = static_cast<size_t>(stage_bytes * (dl ? ns : (dbuf ? 2 : 1)));
   out->fast = fast;
   out->fn = find_gemm_kernel(dtype, L.I, fast ? static_cast<int>(cpr) : 0,
                              static_cast<int>(L.TM), static_cast<int>(L.TN));
@@ -298,6 +310,8 @@ int gt_lower(const gt_config* cfg, int64_t M, int64_t N, int64_t K, int dtype,
   info->TM = static_cast<int32_t>(lw.L.TM);
   info->TN = static_cast<int32_t>(lw.L.TN);
   info->fast = lw.fast ? 1 : 0;
+  info->dl = lw.args.dl;
+  info->ring = lw.args.ns;
   info->waves = static_cast<int32_t>(lw.L.W);
   info->BM = lw.args.BM;
   info->BN = lw.args.BN;

@@ -44,8 +44,8 @@ class gt_config(ctypes.Structure):
 
 class gt_kernel_info(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
-                ("I", "IK", "TM", "TN", "fast", "waves", "BM", "BN", "BK", "dbuf", "acc_regs",
-                 "lds_bytes")] + [("grid_x", ctypes.c_int64), ("grid_y", ctypes.c_int64)]
+                ("I", "IK", "TM", "TN", "fast", "dl", "ring", "waves", "BM", "BN", "BK", "dbuf",
+                 "acc_regs", "lds_bytes")] + [("grid_x", ctypes.c_int64), ("grid_y", ctypes.c_int64)]
 
 
 class gt_log_entry(ctypes.Structure):

@@ -219,3 +219,32 @@ def test_reference_compare_and_measure(gt, orc):
     # early abort: a threshold below any kernel time stops after the warm-up
     m = gt.gt_measure(cfg, Ad, Bd, C, warmup=1, runs=10, abort_ms=1e-9)
     assert m["aborted"] and m["mean_ms"] == m["first_ms"]
+
+
+@pytest.mark.parametrize("shape", [(512, 512, 1024), (256, 768, 512)])
+def test_direct_load_path_bit_exact(gt, orc, shape):
+    """Sampled configurations that lower to the direct-to-LDS ring path (bf16),
+    small-integer inputs: every product must match the oracle bit-exactly."""
+    M, N, K = shape
+    sp = gt.Space(M, N, K, (4, 4, 4), "bf16", True)
+    A, B = make_inputs(M, N, K, "bf16", 13, "smallint")
+    ref = orc.gemm(raw_bytes(A), raw_bytes(B), M, N, K, "bf16")
+    rng = np.random.default_rng(M + N + K)
+    seen, rings, tries = [], set(), 0
+    while len(seen) < 24 and tries < 400000:
+        tries += 1
+        c = sp.unrank(int(rng.integers(0, sp.size())))
+        if not sp.legit(c):
+            continue
+        info = gt.lower(c, M, N, K, "bf16")
+        if not info["dl"]:
+            continue
+        seen.append(c)
+        rings.add(info["ring"])
+    assert len(seen) >= 8 and len(rings) >= 2, (len(seen), rings)
+    for c in seen:
+        info = gt.lower(c, M, N, K, "bf16")
+        note(f"direct-load {shape} {c} ring={info['ring']} W={info['waves']} "
+             f"{info['BM']}x{info['BN']}x{info['BK']} split={info['grid_y']}")
+        C = run(gt, c, A, B)
+        assert np.array_equal(C.astype(np.float64), ref), c
