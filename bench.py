@@ -54,6 +54,46 @@ def fmt_cfg(c):
     return "m{}k{}n{}mfma{}".format(list(c[0]), list(c[1]), list(c[2]), c[3])
 
 
+def kernel_name(w, info):
+    """Symbol of the kernel instantiation a lowered configuration launches."""
+    dt = 1 if w.dtype == "bf16" else 0
+    cpr = info["BK"] // (8 if w.dtype == "bf16" else 4) if info["fast"] else 0
+    return f"gt::gemm_kernel<{dt}, {info['I']}, {info['TM']}, {info['TN']}, {cpr}>"
+
+
+def kernel_source_hash():
+    """Fingerprint of the sources that determine the GEMM kernels' code."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in ("gemm_kernel.hpp", "runtime.cpp", "gemm_inst.hip"):
+        with open(os.path.join(ROOT, "paper_1909_10616_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def launch_signature(w, info):
+    return (f"{w.name} {kernel_name(w, info).replace(' ', '')} grid={info['grid_x']}x{info['grid_y']} "
+            f"waves={info['waves']} lds={info['lds_bytes']} dl={info['dl']}/{info['ring']}")
+
+
+def measured_traffic(w, info):
+    """HBM bytes per launch from profiles/traffic.txt, when the counters were
+    taken on this exact launch signature with the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", "traffic.txt")
+    if not os.path.exists(path):
+        return None
+    want = launch_signature(w, info)
+    src = kernel_source_hash()
+    for line in open(path):
+        if line.startswith("#") or "|" not in line:
+            continue
+        sig, rest = (x.strip() for x in line.split("|", 1))
+        kv = dict(t.split("=", 1) for t in rest.split())
+        if sig == want and kv.get("source") == src:
+            return int(float(kv["traffic_bytes"]))
+    return None
+
+
 def cpu_baseline(w, A, B, target_s: float):
     """The oracle (plain fp64 three-loop GEMM) on host cores, on a bounded
     sample of rows of the same product, in TFLOP/s."""
@@ -91,6 +131,11 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--log-out", default=None, help="write the search log (JSON) here")
+    ap.add_argument("--replay", default=None,
+                    help="skip the search: launch this configuration (JSON) --repeat times")
+    ap.add_argument("--repeat", type=int, default=REPEAT)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="launch a plain device copy of MIB MiB --repeat times (counter scale)")
     args = ap.parse_args()
 
     if args.gpus != 1:
@@ -106,6 +151,16 @@ def main():
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a GPU")
     gt.lib()  # loud failure when the HIP library is missing
+    if args.calibrate_copy:
+        n = args.calibrate_copy << 18  # floats
+        src = torch.ones(n, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(args.repeat):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes_read": n * 4, "bytes_written": n * 4,
+                          "launches": args.repeat}))
+        return
     w = WORKLOADS[args.workload]
     budget = args.budget or w.budget
     dev = torch.device("cuda:0")
@@ -124,6 +179,23 @@ def main():
 
     ev0 = torch.cuda.Event(enable_timing=True)
     ev1 = torch.cuda.Event(enable_timing=True)
+
+    if args.replay:
+        cfg = tuple(tuple(x) if isinstance(x, list) else x for x in json.loads(args.replay))
+        assert sp.legit(cfg), cfg
+        with torch.cuda.stream(stream):
+            gt.gemm_run(cfg, Ad, Bd, C, stream=stream)
+            ev0.record(stream)
+            for _ in range(args.repeat):
+                gt.gemm_run(cfg, Ad, Bd, C, stream=stream)
+            ev1.record(stream)
+            ev1.synchronize()
+        ms = ev0.elapsed_time(ev1) / args.repeat
+        info = gt.lower(cfg, w.M, w.N, w.K, w.dtype)
+        print(json.dumps({"replay": fmt_cfg(cfg), "ms": ms, "tflops": gt.tflops(w.M, w.N, w.K, ms),
+                          "launches": args.repeat + 1, "grid_x": info["grid_x"],
+                          "lds_bytes": info["lds_bytes"]}))
+        return
 
     def step():
         with torch.cuda.stream(stream):
@@ -192,12 +264,14 @@ def main():
             "search_best_cost_ms": last["best_cost"], "best_ms": best_ms,
             "search_wall_s": round(last["wall_s"], 2), "failed": last["failed"],
             "stop": last["stop_reason"], "best_rel_diff_vs_reference": rel,
-            "kernel": {k: info[k] for k in ("I", "TM", "TN", "fast", "waves", "BM", "BN", "BK",
-                                            "dbuf", "lds_bytes", "grid_x", "grid_y")},
+            "kernel": {k: info[k] for k in ("I", "TM", "TN", "fast", "dl", "ring", "waves", "BM",
+                                            "BN", "BK", "dbuf", "lds_bytes", "grid_x", "grid_y")},
+            "kernel_name": kernel_name(w, info), "launch_signature": launch_signature(w, info),
+            "kernel_source": kernel_source_hash(),
         },
         "roofline": {
             "bound": "mfma", "achieved": round(value, 2), "peak": peak, "unit": "TFLOP/s",
-            "frac": round(value / peak, 4), "traffic": None,
+            "frac": round(value / peak, 4), "traffic": measured_traffic(w, info),
             "algorithmic_bytes": alg_bytes,
             "hbm_gbs_at_algorithmic_bytes": round(alg_bytes / (best_ms * 1e-3) / 1e9, 1),
         },

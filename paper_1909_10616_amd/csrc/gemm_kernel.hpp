@@ -596,11 +596,13 @@ constexpr int kMaxDlInst = 16;
 
 // XOR applied to the 16-byte chunk index of B row k in LDS. A transposing
 // read touches rows k0 … k0+3 (k0 ≡ 0 mod 4) and, per 16-lane group, two
-// adjacent chunks (four per 32 lanes); f(k mod 4) ∈ {0, 6, 10, 12} sends those
-// to 8 distinct 16-byte bank slots mod 128 B and 16 distinct mod 256 B.
+// adjacent chunks (four per 32 lanes with 32×32 MFMA; with 16×16 MFMA the
+// second 16-lane group reads rows k0+8 … k0+11 instead). f(k mod 4) ∈
+// {0, 6, 10, 12}, XOR-ed with 8 when bit 3 of k is set, sends those accesses
+// to distinct 16-byte bank slots mod 128 B (16 lanes) and mod 256 B (32 lanes).
 __device__ __forceinline__ int bswz(int k, int cprb) {
   const int j = k & 3;
-  return ((j << 2) | (((j ^ (j >> 1)) & 1) << 1)) & (cprb - 1);
+  return (((j << 2) | (((j ^ (j >> 1)) & 1) << 1)) ^ (((k >> 3) & 1) << 3)) & (cprb - 1);
 }  // direct-load instructions per wavefront per stage
 
 // vmcnt field of s_waitcnt on gfx9: bits [3:0] and [15:14]; lgkmcnt [11:8], expcnt [6:4].
