@@ -58,6 +58,8 @@ def kernel_name(w, info):
     """Symbol of the kernel instantiation a lowered configuration launches."""
     dt = 1 if w.dtype == "bf16" else 0
     cpr = info["BK"] // (8 if w.dtype == "bf16" else 4) if info["fast"] else 0
+    if info["dl"]:
+        return f"gt::gemm_kernel_dl<{info['I']}, {info['TM']}, {info['TN']}, {cpr}>"
     return f"gt::gemm_kernel<{dt}, {info['I']}, {info['TM']}, {info['TN']}, {cpr}>"
 
 

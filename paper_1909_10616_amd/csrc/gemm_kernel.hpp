@@ -592,7 +592,10 @@ __device__ void gemm_fast(const KArgs& a, char* smem) {
 // columns n0 + 4(i & 3) hand lane l four consecutive k of column n0 + l.
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
-constexpr int kMaxDlInst = 16;
+// Direct-load instructions per wavefront and stage the kernel keeps offsets
+// for: 8 where the accumulator size admits 8 wavefronts (the register budget
+// per lane is then 256), 16 otherwise.
+constexpr int dl_inst_cap(int64_t acc) { return acc + 96 <= 256 ? 8 : 16; }
 
 // XOR applied to the 16-byte chunk index of B row k in LDS. A transposing
 // read touches rows k0 … k0+3 (k0 ≡ 0 mod 4) and, per 16-lane group, two
@@ -630,15 +633,33 @@ __device__ __forceinline__ void wait_vm_at_most(int n) {
   else waitcnt_vm<0>();
 }
 
-// One 16-byte-per-lane direct global→LDS load (lane j → LDS byte address
-// lds_base + 16·j). Written as inline assembly so that the compiler does not
-// see an LDS write it would have to wait for before every LDS read (it cannot
-// tell the ring slots apart); the ring's vmcnt accounting is done explicitly.
-__device__ __forceinline__ void dma_load16(const void* src, uint32_t lds_base) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off"
+// One 16-byte-per-lane direct global→LDS load: lane j reads 16 bytes at
+// base + off (base uniform, off this lane's byte offset) and writes them to
+// LDS byte address lds_base + 16·j. Written as inline assembly so that the
+// compiler does not see an LDS write it would have to wait for before every
+// LDS read (it cannot tell the ring slots apart); the ring's vmcnt accounting
+// is done explicitly.
+__device__ __forceinline__ void dma_load16(uint32_t off, uint64_t base, uint32_t lds_base) {
+  // base and lds_base are uniform; reading them from the first lane keeps
+  // them in scalar registers whatever the compiler inferred
+  const uint64_t sb =
+      static_cast<uint64_t>(static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(base)))) |
+      (static_cast<uint64_t>(static_cast<uint32_t>(
+           __builtin_amdgcn_readfirstlane(static_cast<int>(base >> 32))))
+       << 32);
+  asm volatile("s_mov_b32 m0, %2\n\tglobal_load_lds_dwordx4 %0, %1"
                :
-               : "v"(src), "s"(lds_base)
+               : "v"(off), "s"(sb), "s"(__builtin_amdgcn_readfirstlane(static_cast<int>(lds_base)))
                : "memory", "m0");
+}
+
+// A wavefront-uniform pointer as a 64-bit scalar (each half taken from the
+// first active lane and zero-extended).
+__device__ __forceinline__ uint64_t uniform_ptr(const void* p) {
+  const uint64_t b = reinterpret_cast<uintptr_t>(p);
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b)));
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(b >> 32)));
+  return static_cast<uint64_t>(lo) | (static_cast<uint64_t>(hi) << 32);
 }
 
 // Byte offset inside LDS of a pointer into the kernel's dynamic LDS.
@@ -657,6 +678,7 @@ __device__ void gemm_fast_dl(const KArgs& a, char* smem) {
   constexpr int LGCPR = ilog2c<CPR>();
   constexpr int NLINE = CPR >= 8 ? CPR / 8 : 1;
   static_assert(NCS >= 1, "stage shallower than one MFMA K step");
+  constexpr int kMaxDlInst = dl_inst_cap(TM * TN * I * I / 64);
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -683,27 +705,60 @@ __device__ void gemm_fast_dl(const KArgs& a, char* smem) {
   // issues p = w, w + nw, … (A instructions first, then B). Each lane works
   // out the chunk its slot holds: A slot s holds chunk swz(s) (swz is an
   // involution), B slot (k, cs) holds row k, chunk cs ^ bswz(k).
+  // Load instruction p of a stage fills slots p·64 … p·64+63; wavefront w
+  // issues p = w, w + nw, … (A instructions first, then B). Each lane works
+  // out the chunk its slot holds: A slot s holds chunk swz(s) (swz is an
+  // involution), B slot (k, cs) holds row k, chunk cs ^ bswz(k). The lane's
+  // byte offset from the stage's A (or B) origin is the same for every stage,
+  // so it is computed once (it fits 32 bits: BM·K and BK·N are below 2^31).
   const int lgcprb = a.lgBN - 3;
-  const int na_w = pa / nw, nb_w = pb / nw;
-  auto issue = [&](int l, int slot) __attribute__((always_inline)) {
-    const int64_t kbase = (static_cast<int64_t>(l) * a.kSplit + z) * BK;
-    const T* ag = Ag + kbase;
-    const T* bg = Bg + kbase * a.N;
-    u32x4* base = lds + slot * stage;
-    for (int t = 0; t < na_w; ++t) {
-      const int p = wave + t * nw;
-      const int q = swz((p << 6) + lane);
-      const T* src = ag + (q >> LGCPR) * a.K + ((q & (CPR - 1)) << 3);
-      dma_load16(src, __builtin_amdgcn_readfirstlane(lds_off(base + (p << 6))));
-    }
-    u32x4* bbase = base + achunks;
-    for (int t = 0; t < nb_w; ++t) {
-      const int p = wave + t * nw;
-      const int sidx = (p << 6) + lane;
+  const int na_w = pa / nw;
+  uint32_t doff[kMaxDlInst];
+#pragma unroll
+  for (int i = 0; i < kMaxDlInst; ++i) {
+    doff[i] = 0;
+    if (i < na_w) {
+      const int q = swz(((wave + i * nw) << 6) + lane);
+      doff[i] = (static_cast<uint32_t>(q >> LGCPR) * static_cast<uint32_t>(a.K) +
+                 static_cast<uint32_t>((q & (CPR - 1)) << 3)) * 2u;
+    } else if (i < ninst) {
+      const int sidx = ((wave + (i - na_w) * nw) << 6) + lane;
       const int k = sidx >> lgcprb, cs = sidx & (cprb - 1);
-      const T* src = bg + k * a.N + ((cs ^ bswz(k, cprb)) << 3);
-      dma_load16(src, __builtin_amdgcn_readfirstlane(lds_off(bbase + (p << 6))));
+      doff[i] = (static_cast<uint32_t>(k) * static_cast<uint32_t>(a.N) +
+                 static_cast<uint32_t>((cs ^ bswz(k, cprb)) << 3)) * 2u;
     }
+  }
+  const int lds0 = __builtin_amdgcn_readfirstlane(static_cast<int>(lds_off(lds)));
+  // Instruction i (< ninst) of this wavefront for stage l into ring slot `slot`.
+  // Instruction i (< ninst) of this wavefront for stage l into ring slot
+  // `slot`; ga, gb: the stage's A and B origins as uniform scalars.
+  auto dma = [&](uint64_t ga, uint64_t gb, uint32_t sbase, int i) __attribute__((always_inline)) {
+    if (i < na_w)
+      dma_load16(doff[i], ga, sbase + static_cast<uint32_t>(wave + i * nw) * 1024u);
+    else
+      dma_load16(doff[i], gb,
+                 sbase + static_cast<uint32_t>(achunks + ((wave + (i - na_w) * nw) << 6)) * 16u);
+  };
+  // Uniform origins of stage l's A and B tiles and LDS byte base of ring slot `slot`.
+  struct StageBase {
+    uint64_t ga, gb;
+    uint32_t sb;
+  };
+  auto stage_base = [&](int l, int slot) __attribute__((always_inline)) {
+    const int64_t kbase = (static_cast<int64_t>(l) * a.kSplit + z) * BK;
+    StageBase r;
+    r.ga = uniform_ptr(Ag + kbase);
+    r.gb = uniform_ptr(Bg + kbase * a.N);
+    r.sb = static_cast<uint32_t>(
+        __builtin_amdgcn_readfirstlane(static_cast<int>(lds0 + slot * stage * 16)));
+    return r;
+  };
+  // All of this wavefront's instructions of stage l, back to back.
+  auto issue = [&](int l, int slot) __attribute__((always_inline)) {
+    const StageBase b = stage_base(l, slot);
+#pragma unroll
+    for (int i = 0; i < kMaxDlInst; ++i)
+      if (i < ninst) dma(b.ga, b.gb, b.sb, i);
   };
 
   acc_t acc[TM][TN];
@@ -755,31 +810,70 @@ __device__ void gemm_fast_dl(const KArgs& a, char* smem) {
       fb[fs][t] = __builtin_bit_cast(u32x4, __builtin_shufflevector(h[0], h[1], 0, 1, 2, 3, 4, 5, 6, 7));
     }
   };
+  auto mfma1 = [&](int fs, int q) __attribute__((always_inline)) {
+    const int i = q / TN, j = q % TN;
+    acc[i][j] = mfma_bf16(__builtin_bit_cast(bf16x8, fa[fs][i]),
+                          __builtin_bit_cast(bf16x8, fb[fs][j]), acc[i][j]);
+  };
   auto mfmas = [&](int fs) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-        acc[i][j] = mfma_bf16(__builtin_bit_cast(bf16x8, fa[fs][i]),
-                              __builtin_bit_cast(bf16x8, fb[fs][j]), acc[i][j]);
+    for (int q = 0; q < TM * TN; ++q) mfma1(fs, q);
   };
 
-  // Ring schedule: stages 0 … ns−1 are issued up front; at the boundary after
-  // stage l's last LDS reads, stage l + ns is issued into stage l's slot. The
-  // boundary (wait for stage l + 1, barrier, issue, first fragments of stage
-  // l + 1) sits in front of stage l's last chunk-step of MFMAs, which then
-  // overlap it.
-  for (int l = 0; l < ns && l < a.kLoop; ++l) issue(l, l);
-  wait_vm_at_most(__builtin_amdgcn_readfirstlane(min(ns - 1, a.kLoop - 1) * ninst));
+  // Ring schedule: stages 0 … ns−2 are issued up front. While stage l is
+  // computed from slot l mod ns, stage l + ns − 1 is loaded into slot
+  // (l − 1) mod ns, which every wavefront stopped reading before the barrier
+  // that ended stage l − 1. Its ninst instructions go one at a time between
+  // the MFMAs of chunk-steps 0 … NCS−2 (one after every R-th MFMA), all
+  // before stage l's own boundary: a wavefront waiting for
+  // room in the memory pipeline cannot issue MFMAs, so loads go out in small
+  // doses. The boundary (wait for stage l + 1, barrier, first fragments of
+  // stage l + 1) sits in front of stage l's last chunk-step of MFMAs.
+  constexpr int TMTN = TM * TN;
+  constexpr int SPOS = NCS > 1 ? (NCS - 1) * TMTN : 0;  // MFMA slots before the boundary
+  const int npro = min(ns - 1, a.kLoop);
+  for (int l = 0; l < npro; ++l) issue(l, l);
+  wait_vm_at_most(__builtin_amdgcn_readfirstlane((npro - 1) * ninst));
   __builtin_amdgcn_s_barrier();
   load_frags(lds, 0, 0);
+  // one load after every R-th MFMA slot: the kernel's instruction cap spread evenly
+  constexpr int R = SPOS / kMaxDlInst > 1 ? SPOS / kMaxDlInst : 1;
   for (int l = 0; l < a.kLoop; ++l) {
     const int cur = l % ns;
     const u32x4* as = lds + cur * stage;
+    const int ld = l + ns - 1;  // stage loaded during this one
+    const bool load = ld < a.kLoop;
+    StageBase sbs{0, 0, 0};
+    if (load) sbs = stage_base(ld, ld % ns);
+    if constexpr (NCS == 1) {
+      if (load) {
+#pragma unroll
+        for (int i = 0; i < kMaxDlInst; ++i)
+          if (i < ninst) dma(sbs.ga, sbs.gb, sbs.sb, i);
+      }
+    }
 #pragma unroll
     for (int cs = 0; cs + 1 < NCS; ++cs) {
       load_frags(as, cs + 1, (cs + 1) & 1);
-      mfmas(cs & 1);
+#pragma unroll
+      for (int q = 0; q < TMTN; ++q) {
+        mfma1(cs & 1, q);
+        const int pos = cs * TMTN + q;
+        const int i = pos / R;
+        if (pos % R == R - 1 && i < kMaxDlInst) {
+          if (load && i < ninst) {
+            __builtin_amdgcn_sched_barrier(0);
+            dma(sbs.ga, sbs.gb, sbs.sb, i);
+            __builtin_amdgcn_sched_barrier(0);
+          }
+        }
+      }
+    }
+    if constexpr (NCS > 1) {
+      // instructions beyond the MFMA slots (ninst > SPOS)
+#pragma unroll
+      for (int i = SPOS / R; i < kMaxDlInst; ++i)
+        if (load && i < ninst) dma(sbs.ga, sbs.gb, sbs.sb, i);
     }
     const bool more = l + 1 < a.kLoop;
     const u32x4* nx = lds + ((l + 1) % ns) * stage;
@@ -789,7 +883,6 @@ __device__ void gemm_fast_dl(const KArgs& a, char* smem) {
       waitcnt_lgkm0();  // this wavefront's reads of slot cur are complete
       // every wavefront: stage l + 1 landed, done reading slot cur
       __builtin_amdgcn_s_barrier();
-      if (l + ns < a.kLoop) issue(l + ns, cur);
       if constexpr (NCS >= 2) load_frags(nx, 0, 0);  // the last chunk-step uses slot 1
     }
     mfmas((NCS - 1) & 1);
@@ -832,24 +925,26 @@ template <int DT, int I, int TM, int TN, int CPR>
 __global__ void __launch_bounds__((launch_threads<I, TM, TN, CPR>())) gemm_kernel(KArgs a) {
   extern __shared__ u32x4 gt_smem[];
   char* smem = reinterpret_cast<char*>(gt_smem);
-  if constexpr (CPR > 0 && DT == 1) {
-    if (a.dl)
-      gemm_fast_dl<I, TM, TN, CPR>(a, smem);
-    else
-      gemm_fast<DT, I, TM, TN, CPR>(a, smem);
-  } else if constexpr (CPR > 0)
+  if constexpr (CPR > 0)
     gemm_fast<DT, I, TM, TN, CPR>(a, smem);
   else
     gemm_generic<DT, I, TM, TN>(a, smem);
 }
 
+// bf16 fast path with direct global→LDS loads: a kernel of its own, so that
+// its register allocation does not inherit the register-staged path's.
+template <int I, int TM, int TN, int CPR>
+__global__ void __launch_bounds__((launch_threads<I, TM, TN, CPR>())) gemm_kernel_dl(KArgs a) {
+  extern __shared__ u32x4 gt_smem[];
+  gemm_fast_dl<I, TM, TN, CPR>(a, reinterpret_cast<char*>(gt_smem));
+}
+
 using LaunchFn = hipError_t (*)(const KArgs&, dim3, dim3, size_t, hipStream_t);
 
-template <int DT, int I, int TM, int TN, int CPR>
-hipError_t launch_gemm(const KArgs& a, dim3 grid, dim3 block, size_t lds, hipStream_t s) {
-  auto fn = gemm_kernel<DT, I, TM, TN, CPR>;
-  static bool attr_set = false;  // raise the dynamic LDS limit once per kernel
-  if (!attr_set) {
+template <class F>
+hipError_t launch_one(F fn, bool& attr_set, const KArgs& a, dim3 grid, dim3 block, size_t lds,
+                      hipStream_t s) {
+  if (!attr_set) {  // raise the dynamic LDS limit once per kernel
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
                                        hipFuncAttributeMaxDynamicSharedMemorySize, 163840);
     if (e != hipSuccess) return e;
@@ -857,6 +952,18 @@ hipError_t launch_gemm(const KArgs& a, dim3 grid, dim3 block, size_t lds, hipStr
   }
   hipLaunchKernelGGL(fn, grid, block, lds, s, a);
   return hipGetLastError();
+}
+
+template <int DT, int I, int TM, int TN, int CPR>
+hipError_t launch_gemm(const KArgs& a, dim3 grid, dim3 block, size_t lds, hipStream_t s) {
+  if constexpr (DT == 1 && CPR > 0) {
+    if (a.dl) {
+      static bool attr_dl = false;
+      return launch_one(gemm_kernel_dl<I, TM, TN, CPR>, attr_dl, a, grid, block, lds, s);
+    }
+  }
+  static bool attr = false;
+  return launch_one(gemm_kernel<DT, I, TM, TN, CPR>, attr, a, grid, block, lds, s);
 }
 
 // (TM, TN) pairs with TM·TN ≤ 16 (I = 32) and ≤ 64 (I = 16): the register

@@ -70,12 +70,13 @@ int lower(const gt_config& c, int64_t M, int64_t N, int64_t K, int dtype, const 
   const bool dbuf = L.kLoop >= 2 && 2 * stage_bytes <= kLdsMax;
   // bf16 fast path with direct global->LDS loads into a ring of ns stages:
   // whole 64-slot load instructions, an even split over the wavefronts, at
-  // most 16 instructions per wavefront and stage, 32-bit element offsets
+  // most dl_inst_cap(acc) instructions per wavefront and stage, 32-bit
+  // element offsets
   const int64_t achunks = L.BM * L.BK / 8, bchunks = L.BK * L.BN / 8;
   const int64_t dl_inst = (achunks + bchunks) / 64;
   const int64_t ns = std::min<int64_t>(8, kLdsMax / std::max<int64_t>(stage_bytes, 1));
   const bool dl = fast && dtype == GT_BF16 && achunks % (64 * L.W) == 0 &&
-                  bchunks % (64 * L.W) == 0 && dl_inst / L.W <= 16 && ns >= 2 &&
+                  bchunks % (64 * L.W) == 0 && dl_inst / L.W <= dl_inst_cap(L.acc) && ns >= 2 &&
                   L.BM * K < (int64_t{1} << 31) && L.BK * N < (int64_t{1} << 31);
 
   KArgs& a = out->args;

@@ -11,6 +11,11 @@
       HBM traffic per launch: FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of the
       kernel, each scaled by (known copy bytes / what the same counter reads for
       a plain device copy of that size).
+  python -m paper_1909_10616_amd.profsum bestcfg BENCH_JSON
+      the best configuration of a bench line, as the JSON bench.py --replay takes.
+  python -m paper_1909_10616_amd.profsum report OUT
+      markdown summary of a profile_bench.sh output folder, ending with the
+      line for profiles/traffic.txt.
 """
 from __future__ import annotations
 
@@ -18,7 +23,9 @@ import argparse
 import collections
 import csv
 import glob
+import json
 import os
+import re
 import statistics
 
 
@@ -99,9 +106,100 @@ def traffic(fetch_dir, write_dir, cfetch_dir, cwrite_dir, copy_bytes, kernel, gr
             "traffic_bytes": f_k * 1024.0 * ff + w_k * 1024.0 * wf}
 
 
+def best_cfg(bench_json):
+    d = json.load(open(bench_json))
+    m = re.match(r"m(\[.*?\])k(\[.*?\])n(\[.*?\])mfma(\d+)", d["config"]["best_config"])
+    return [json.loads(m.group(1)), json.loads(m.group(2)), json.loads(m.group(3)), int(m.group(4))]
+
+
+def _last_line_json(path):
+    with open(path) as f:
+        lines = [l for l in f if l.strip().startswith("{")]
+    return json.loads(lines[-1])
+
+
+def report(out, copy_bytes=1 << 30):
+    b = _last_line_json(os.path.join(out, "bench_traced.json"))
+    c = b["config"]
+    kname = c["kernel_name"]
+    info = c["kernel"]
+    grid = info["grid_x"] * 64 * info["waves"]
+    rows = [r for r in _rows(os.path.join(out, "trace"), "bench", "kernel_trace")]
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    sel = [r for r in rows if _match(r, kname, grid, info["lds_bytes"])
+           and int(r.get("Grid_Size_Y") or 1) == info["grid_y"]]
+    last = sel[-200:]
+    dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in last]
+    t = traffic(*(os.path.join(out, d) for d in ("fetch", "write", "cfetch", "cwrite")),
+                copy_bytes, kname, grid, info["lds_bytes"])
+    u, _ = pmc(os.path.join(out, "util"), "u", kname, grid, info["lds_bytes"])
+    uc = {cn: v for (k, cn), v in u.items()}
+    w = c["workload"]
+    flops = 2.0 * c["M"] * c["N"] * c["K"]
+    mean_us = statistics.mean(dur)
+    L = []
+    L.append(f"# {w}: {kname}, {info['BM']}x{info['BN']}x{info['BK']} tile, {info['waves']} wavefronts")
+    L.append("")
+    L.append("Commands (from the repository root on the GPU host; OUT is the output folder):")
+    L.append("")
+    L.append("    paper_1909_10616_amd/profile_bench.sh OUT")
+    L.append("      = rocprofv3 --kernel-trace --stats --output-format csv -d OUT/trace -o bench -- "
+             "python3 bench.py --no-cpu-baseline")
+    L.append("        rocprofv3 --pmc FETCH_SIZE   (then WRITE_SIZE) ... -- python3 bench.py --replay CFG --repeat 20")
+    L.append("        rocprofv3 --pmc FETCH_SIZE   (then WRITE_SIZE) ... -- python3 bench.py --calibrate-copy 1024 --repeat 5")
+    L.append("        rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_LDS_BANK_CONFLICT "
+             "SQ_LDS_IDX_ACTIVE SQ_WAVE_CYCLES SQ_WAIT_ANY ... -- python3 bench.py --replay CFG --repeat 20")
+    L.append("    python3 paper_1909_10616_amd/profsum.py report OUT")
+    L.append("")
+    L.append(f"Best configuration of the traced search: `{c['best_config']}` (CFG), "
+             f"{c['configs_timed']} configurations timed of {c['space_size']} "
+             f"({c['fraction_of_space_pct']:.6f}% of the space), search {c['search_wall_s']} s.")
+    L.append(f"Launch: `{c['launch_signature']}`, kernel sources `{c['kernel_source']}`.")
+    if last:
+        r0 = last[-1]
+        L.append(f"Registers per lane: {r0.get('VGPR_Count')} VGPR + {r0.get('Accum_VGPR_Count')} AGPR, "
+                 f"{r0.get('SGPR_Count')} SGPR; scratch {r0.get('Scratch_Size')} B.")
+    L.append("")
+    L.append("## Kernel trace vs. bench timing")
+    L.append("")
+    L.append("| source | launches | mean µs | TFLOP/s |")
+    L.append("|---|---|---|---|")
+    L.append(f"| kernel trace, last {len(dur)} dispatches of CFG | {len(dur)} | {mean_us:.2f} | "
+             f"{flops / (mean_us * 1e-6) / 1e12:.1f} |")
+    L.append(f"| bench.py HIP events around the same {len(dur)} launches (best_ms) | {len(dur)} | "
+             f"{b['config']['best_ms'] * 1e3:.2f} | {b['value']:.1f} |")
+    L.append(f"| median of the traced dispatches | | {statistics.median(dur):.2f} | |")
+    L.append("")
+    L.append(f"Fraction of MFMA peak ({b['roofline']['peak']} TFLOP/s): {b['roofline']['frac']:.4f}.")
+    L.append("")
+    L.append("## HBM traffic per launch (FETCH_SIZE, WRITE_SIZE; scaled by a 1 GiB copy)")
+    L.append("")
+    L.append("| counter | kernel KiB/dispatch | copy KiB/dispatch | scale | bytes |")
+    L.append("|---|---|---|---|---|")
+    L.append(f"| FETCH_SIZE | {t['fetch_kib']:.0f} | {t['copy_fetch_kib']:.0f} | {t['fetch_factor']:.3f} | "
+             f"{t['fetch_bytes']:.4g} |")
+    L.append(f"| WRITE_SIZE | {t['write_kib']:.0f} | {t['copy_write_kib']:.0f} | {t['write_factor']:.3f} | "
+             f"{t['write_bytes']:.4g} |")
+    alg = b["roofline"]["algorithmic_bytes"]
+    L.append("")
+    L.append(f"Total {t['traffic_bytes']:.4g} B per launch against {alg} algorithmic bytes "
+             f"(A and B read once, C written once): {t['traffic_bytes'] / alg:.2f}x. "
+             f"At the traced mean that is {t['traffic_bytes'] / (mean_us * 1e-6) / 1e9:.0f} GB/s of HBM.")
+    L.append("")
+    L.append("## Utilisation counters (mean per dispatch of CFG)")
+    L.append("")
+    for k in sorted(uc):
+        L.append(f"- {k}: {uc[k]:.0f}")
+    L.append("")
+    L.append("## Line for profiles/traffic.txt")
+    L.append("")
+    L.append(f"    {c['launch_signature']} | source={c['kernel_source']} traffic_bytes={t['traffic_bytes']:.0f}")
+    return "\n".join(L)
+
+
 def main():
     ap = argparse.ArgumentParser()
-    ap.add_argument("mode", choices=["trace", "pmc", "traffic"])
+    ap.add_argument("mode", choices=["trace", "pmc", "traffic", "bestcfg", "report"])
     ap.add_argument("dirs", nargs="+")
     ap.add_argument("--kernel", default=None)
     ap.add_argument("--grid", type=int, default=0)
@@ -110,7 +208,11 @@ def main():
     ap.add_argument("--copy-bytes", type=float, default=0)
     ap.add_argument("--copy-kernel", default="copy")
     a = ap.parse_args()
-    if a.mode == "trace":
+    if a.mode == "bestcfg":
+        print(json.dumps(best_cfg(a.dirs[0])))
+    elif a.mode == "report":
+        print(report(a.dirs[0]))
+    elif a.mode == "trace":
         print(trace(a.dirs[0], a.dirs[1], a.kernel, a.grid, a.lds, a.last))
     elif a.mode == "pmc":
         vals, n = pmc(a.dirs[0], a.dirs[1], a.kernel, a.grid, a.lds)
