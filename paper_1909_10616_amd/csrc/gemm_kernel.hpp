@@ -820,60 +820,66 @@ __device__ void gemm_fast_dl(const KArgs& a, char* smem) {
     for (int q = 0; q < TM * TN; ++q) mfma1(fs, q);
   };
 
-  // Ring schedule: stages 0 … ns−2 are issued up front. While stage l is
-  // computed from slot l mod ns, stage l + ns − 1 is loaded into slot
-  // (l − 1) mod ns, which every wavefront stopped reading before the barrier
-  // that ended stage l − 1. Its ninst instructions go one at a time between
-  // the MFMAs of chunk-steps 0 … NCS−2 (one after every R-th MFMA), all
-  // before stage l's own boundary: a wavefront waiting for
-  // room in the memory pipeline cannot issue MFMAs, so loads go out in small
-  // doses. The boundary (wait for stage l + 1, barrier, first fragments of
-  // stage l + 1) sits in front of stage l's last chunk-step of MFMAs.
+  // Ring schedule. Stage s is loaded into slot s mod ns. Its loads are issued
+  // in a window of NCS chunk-steps of MFMAs: the last chunk-step of stage
+  // s − ns (which runs after the barrier that ends stage s − ns, once every
+  // wavefront has stopped reading slot s mod ns) and chunk-steps 0 … NCS−2 of
+  // stage s − ns + 1, so the whole set is out before the boundary that ends
+  // stage s − ns + 1. Inside the window the wavefront's ninst instructions go
+  // one at a time, one after every R-th MFMA: a wavefront waiting for room in
+  // the memory pipeline cannot issue MFMAs, so loads go out in small doses,
+  // and the last of them leaves half a chunk-step before the window closes.
+  // Stages 0 … ns−2 (and the part of stage ns − 1's window that would precede
+  // stage 0) are issued up front. The boundary (wait for stage l + 1, barrier,
+  // first fragments of stage l + 1) sits in front of stage l's last
+  // chunk-step of MFMAs.
   constexpr int TMTN = TM * TN;
-  constexpr int SPOS = NCS > 1 ? (NCS - 1) * TMTN : 0;  // MFMA slots before the boundary
+  constexpr int SPOS = NCS * TMTN;  // MFMA slots in a window
+  constexpr int RR = (SPOS - TMTN / 2) / kMaxDlInst;
+  constexpr int R = RR > 1 ? RR : 1;
+  // load i of a window goes after MFMA slot i·R + R − 1; slots past the window
+  // (ninst·R > SPOS) go out with the window's last slot
+  auto dma_at = [&](const StageBase& sb, bool on, int pos) __attribute__((always_inline)) {
+    const int i = pos / R;
+    if (pos % R == R - 1 && i < kMaxDlInst && i * R + R - 1 < SPOS) {
+      if (on && i < ninst) {
+        __builtin_amdgcn_sched_barrier(0);
+        dma(sb.ga, sb.gb, sb.sb, i);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    if (pos == SPOS - 1) {
+#pragma unroll
+      for (int j = SPOS / R; j < kMaxDlInst; ++j)
+        if (on && j < ninst) dma(sb.ga, sb.gb, sb.sb, j);
+    }
+  };
   const int npro = min(ns - 1, a.kLoop);
   for (int l = 0; l < npro; ++l) issue(l, l);
   wait_vm_at_most(__builtin_amdgcn_readfirstlane((npro - 1) * ninst));
   __builtin_amdgcn_s_barrier();
+  if (ns - 1 < a.kLoop) {
+    // the part of stage ns − 1's window before stage 0 (slot ns − 1 is unused so far)
+    const StageBase sb0 = stage_base(ns - 1, ns - 1);
+#pragma unroll
+    for (int pos = 0; pos < TMTN; ++pos) dma_at(sb0, true, pos);
+  }
   load_frags(lds, 0, 0);
-  // one load after every R-th MFMA slot: the kernel's instruction cap spread evenly
-  constexpr int R = SPOS / kMaxDlInst > 1 ? SPOS / kMaxDlInst : 1;
   for (int l = 0; l < a.kLoop; ++l) {
     const int cur = l % ns;
     const u32x4* as = lds + cur * stage;
-    const int ld = l + ns - 1;  // stage loaded during this one
+    const int ld = l + ns - 1;  // stage whose window ends with this stage's boundary
     const bool load = ld < a.kLoop;
     StageBase sbs{0, 0, 0};
-    if (load) sbs = stage_base(ld, ld % ns);
-    if constexpr (NCS == 1) {
-      if (load) {
-#pragma unroll
-        for (int i = 0; i < kMaxDlInst; ++i)
-          if (i < ninst) dma(sbs.ga, sbs.gb, sbs.sb, i);
-      }
-    }
+    if (load && NCS > 1) sbs = stage_base(ld, ld % ns);
 #pragma unroll
     for (int cs = 0; cs + 1 < NCS; ++cs) {
       load_frags(as, cs + 1, (cs + 1) & 1);
 #pragma unroll
       for (int q = 0; q < TMTN; ++q) {
         mfma1(cs & 1, q);
-        const int pos = cs * TMTN + q;
-        const int i = pos / R;
-        if (pos % R == R - 1 && i < kMaxDlInst) {
-          if (load && i < ninst) {
-            __builtin_amdgcn_sched_barrier(0);
-            dma(sbs.ga, sbs.gb, sbs.sb, i);
-            __builtin_amdgcn_sched_barrier(0);
-          }
-        }
+        dma_at(sbs, load, TMTN + cs * TMTN + q);
       }
-    }
-    if constexpr (NCS > 1) {
-      // instructions beyond the MFMA slots (ninst > SPOS)
-#pragma unroll
-      for (int i = SPOS / R; i < kMaxDlInst; ++i)
-        if (load && i < ninst) dma(sbs.ga, sbs.gb, sbs.sb, i);
     }
     const bool more = l + 1 < a.kLoop;
     const u32x4* nx = lds + ((l + 1) % ns) * stage;
@@ -885,7 +891,15 @@ __device__ void gemm_fast_dl(const KArgs& a, char* smem) {
       __builtin_amdgcn_s_barrier();
       if constexpr (NCS >= 2) load_frags(nx, 0, 0);  // the last chunk-step uses slot 1
     }
-    mfmas((NCS - 1) & 1);
+    // last chunk-step; its slots open the window of stage l + ns (into slot cur)
+    const bool load2 = l + ns < a.kLoop;
+    StageBase sb2{0, 0, 0};
+    if (load2) sb2 = stage_base(l + ns, cur);
+#pragma unroll
+    for (int q = 0; q < TMTN; ++q) {
+      mfma1((NCS - 1) & 1, q);
+      dma_at(sb2, load2, q);
+    }
     if constexpr (NCS == 1) {
       if (more) load_frags(nx, 0, 0);
     }
