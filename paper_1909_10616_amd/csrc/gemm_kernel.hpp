@@ -704,10 +704,6 @@ __device__ void gemm_fast_dl(const KArgs& a, char* smem) {
   // Load instruction p of a stage fills slots p·64 … p·64+63; wavefront w
   // issues p = w, w + nw, … (A instructions first, then B). Each lane works
   // out the chunk its slot holds: A slot s holds chunk swz(s) (swz is an
-  // involution), B slot (k, cs) holds row k, chunk cs ^ bswz(k).
-  // Load instruction p of a stage fills slots p·64 … p·64+63; wavefront w
-  // issues p = w, w + nw, … (A instructions first, then B). Each lane works
-  // out the chunk its slot holds: A slot s holds chunk swz(s) (swz is an
   // involution), B slot (k, cs) holds row k, chunk cs ^ bswz(k). The lane's
   // byte offset from the stage's A (or B) origin is the same for every stage,
   // so it is computed once (it fits 32 bits: BM·K and BK·N are below 2^31).
@@ -729,7 +725,6 @@ __device__ void gemm_fast_dl(const KArgs& a, char* smem) {
     }
   }
   const int lds0 = __builtin_amdgcn_readfirstlane(static_cast<int>(lds_off(lds)));
-  // Instruction i (< ninst) of this wavefront for stage l into ring slot `slot`.
   // Instruction i (< ninst) of this wavefront for stage l into ring slot
   // `slot`; ga, gb: the stage's A and B origins as uniform scalars.
   auto dma = [&](uint64_t ga, uint64_t gb, uint32_t sbase, int i) __attribute__((always_inline)) {

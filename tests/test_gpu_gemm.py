@@ -157,6 +157,9 @@ FULL = [
     ("gemm4096_bf16", ((16, 2, 4, 32), (64, 1, 4, 16), (16, 2, 4, 32), 32)),
     ("gemm4096_bf16", ((32, 2, 2, 32), (64, 1, 2, 32), (16, 2, 4, 32), 32)),
     ("gemm4096_bf16", ((32, 2, 4, 16), (128, 1, 1, 32), (32, 2, 4, 16), 16)),
+    # 256x256x32 tiles, 8 wavefronts, direct-load ring of 5 stages (both MFMA sizes)
+    ("gemm4096_bf16", ((16, 4, 2, 32), (128, 1, 2, 16), (16, 2, 4, 32), 32)),
+    ("gemm4096_bf16", ((16, 2, 8, 16), (128, 1, 1, 32), (16, 4, 1, 64), 16)),
     ("mlp4096x11008x4096_bf16", ((16, 2, 4, 32), (64, 1, 4, 16), (43, 2, 4, 32), 32)),
     ("skinny64x4096x4096_bf16", ((1, 1, 2, 32), (16, 8, 2, 16), (32, 2, 2, 32), 32)),
     ("gemm1024_f32", ((8, 2, 2, 32), (32, 1, 4, 8), (8, 2, 2, 32), 0)),
@@ -248,3 +251,4 @@ def test_direct_load_path_bit_exact(gt, orc, shape):
              f"{info['BM']}x{info['BN']}x{info['BK']} split={info['grid_y']}")
         C = run(gt, c, A, B)
         assert np.array_equal(C.astype(np.float64), ref), c
+
