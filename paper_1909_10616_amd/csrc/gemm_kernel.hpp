@@ -669,7 +669,7 @@ __device__ __forceinline__ uint32_t lds_off(const void* p) {
 }
 
 template <int I, int TM, int TN, int CPR>
-__device__ void gemm_fast_dl(const KArgs& a, char* smem) {
+__device__ __forceinline__ void gemm_fast_dl(const KArgs& a, char* smem) {
   using T = uint16_t;
   using acc_t = typename AccT<I>::type;
   constexpr int NACC = AccT<I>::N;
@@ -727,12 +727,12 @@ __device__ void gemm_fast_dl(const KArgs& a, char* smem) {
   const int lds0 = __builtin_amdgcn_readfirstlane(static_cast<int>(lds_off(lds)));
   // Instruction i (< ninst) of this wavefront for stage l into ring slot
   // `slot`; ga, gb: the stage's A and B origins as uniform scalars.
+  // A or B is picked with scalar selects, not branches.
   auto dma = [&](uint64_t ga, uint64_t gb, uint32_t sbase, int i) __attribute__((always_inline)) {
-    if (i < na_w)
-      dma_load16(doff[i], ga, sbase + static_cast<uint32_t>(wave + i * nw) * 1024u);
-    else
-      dma_load16(doff[i], gb,
-                 sbase + static_cast<uint32_t>(achunks + ((wave + (i - na_w) * nw) << 6)) * 16u);
+    const bool isa = i < na_w;
+    const uint32_t da = static_cast<uint32_t>(wave + i * nw) * 1024u;
+    const uint32_t db = static_cast<uint32_t>(achunks + ((wave + (i - na_w) * nw) << 6)) * 16u;
+    dma_load16(doff[i], isa ? ga : gb, sbase + (isa ? da : db));
   };
   // Uniform origins of stage l's A and B tiles and LDS byte base of ring slot `slot`.
   struct StageBase {
@@ -830,75 +830,96 @@ __device__ void gemm_fast_dl(const KArgs& a, char* smem) {
   // chunk-step of MFMAs.
   constexpr int TMTN = TM * TN;
   constexpr int SPOS = NCS * TMTN;  // MFMA slots in a window
-  constexpr int RR = (SPOS - TMTN / 2) / kMaxDlInst;
-  constexpr int R = RR > 1 ? RR : 1;
-  // load i of a window goes after MFMA slot i·R + R − 1; slots past the window
-  // (ninst·R > SPOS) go out with the window's last slot
-  auto dma_at = [&](const StageBase& sb, bool on, int pos) __attribute__((always_inline)) {
-    const int i = pos / R;
-    if (pos % R == R - 1 && i < kMaxDlInst && i * R + R - 1 < SPOS) {
-      if (on && i < ninst) {
-        __builtin_amdgcn_sched_barrier(0);
-        dma(sb.ga, sb.gb, sb.sb, i);
-        __builtin_amdgcn_sched_barrier(0);
+  // The loop is instantiated for NI = cap and cap/2 instructions per
+  // wavefront and stage (NI = 0: any other count, guarded per load), so the
+  // common cases carry no per-load branch. Load i of a window goes after MFMA
+  // slot i·R + R − 1 (slots past the window go out with its last slot); R
+  // spreads NI loads so that the last leaves half a chunk-step before the
+  // window closes. Both parts of every window use the same R.
+  auto run = [&](auto ni) __attribute__((always_inline)) {
+    constexpr int NI = decltype(ni)::value;
+    constexpr int NIE = NI ? NI : kMaxDlInst;
+    constexpr int RR = (SPOS - TMTN / 2) / NIE;
+    constexpr int R = RR > 1 ? RR : 1;
+    // open: the window is open for every load of this stage (no guard on it)
+    auto dma_at = [&](const StageBase& sb, bool on, int pos, auto open) __attribute__((always_inline)) {
+      constexpr bool OPEN = decltype(open)::value;
+      const int i = pos / R;
+      if (pos % R == R - 1 && i < NIE && i * R + R - 1 < SPOS) {
+        if ((OPEN || on) && (NI > 0 || i < ninst)) {
+          __builtin_amdgcn_sched_barrier(0);
+          dma(sb.ga, sb.gb, sb.sb, i);
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
+      if (pos == SPOS - 1) {
+#pragma unroll
+        for (int j = SPOS / R; j < NIE; ++j)
+          if ((OPEN || on) && (NI > 0 || j < ninst)) dma(sb.ga, sb.gb, sb.sb, j);
+      }
+    };
+    const int npro = min(ns - 1, a.kLoop);
+    for (int l = 0; l < npro; ++l) issue(l, l);
+    wait_vm_at_most(__builtin_amdgcn_readfirstlane((npro - 1) * ninst));
+    __builtin_amdgcn_s_barrier();
+    if (ns - 1 < a.kLoop) {
+      // the part of stage ns − 1's window before stage 0 (slot ns − 1 is unused so far)
+      const StageBase sb0 = stage_base(ns - 1, ns - 1);
+#pragma unroll
+      for (int pos = 0; pos < TMTN; ++pos) dma_at(sb0, true, pos, std::true_type{});
     }
-    if (pos == SPOS - 1) {
+    load_frags(lds, 0, 0);
+    // One stage; OPEN: both windows it touches are open (all but the last ns stages).
+    auto stage_step = [&](int l, auto open) __attribute__((always_inline)) {
+      constexpr bool OPEN = decltype(open)::value;
+      const int cur = l % ns;
+      const u32x4* as = lds + cur * stage;
+      const int ld = l + ns - 1;  // stage whose window ends with this stage's boundary
+      const bool load = OPEN || ld < a.kLoop;
+      StageBase sbs{0, 0, 0};
+      if (load && NCS > 1) sbs = stage_base(ld, ld % ns);
 #pragma unroll
-      for (int j = SPOS / R; j < kMaxDlInst; ++j)
-        if (on && j < ninst) dma(sb.ga, sb.gb, sb.sb, j);
-    }
-  };
-  const int npro = min(ns - 1, a.kLoop);
-  for (int l = 0; l < npro; ++l) issue(l, l);
-  wait_vm_at_most(__builtin_amdgcn_readfirstlane((npro - 1) * ninst));
-  __builtin_amdgcn_s_barrier();
-  if (ns - 1 < a.kLoop) {
-    // the part of stage ns − 1's window before stage 0 (slot ns − 1 is unused so far)
-    const StageBase sb0 = stage_base(ns - 1, ns - 1);
+      for (int cs = 0; cs + 1 < NCS; ++cs) {
+        load_frags(as, cs + 1, (cs + 1) & 1);
 #pragma unroll
-    for (int pos = 0; pos < TMTN; ++pos) dma_at(sb0, true, pos);
-  }
-  load_frags(lds, 0, 0);
-  for (int l = 0; l < a.kLoop; ++l) {
-    const int cur = l % ns;
-    const u32x4* as = lds + cur * stage;
-    const int ld = l + ns - 1;  // stage whose window ends with this stage's boundary
-    const bool load = ld < a.kLoop;
-    StageBase sbs{0, 0, 0};
-    if (load && NCS > 1) sbs = stage_base(ld, ld % ns);
-#pragma unroll
-    for (int cs = 0; cs + 1 < NCS; ++cs) {
-      load_frags(as, cs + 1, (cs + 1) & 1);
+        for (int q = 0; q < TMTN; ++q) {
+          mfma1(cs & 1, q);
+          dma_at(sbs, load, TMTN + cs * TMTN + q, open);
+        }
+      }
+      const bool more = OPEN || l + 1 < a.kLoop;
+      const u32x4* nx = lds + ((l + 1) % ns) * stage;
+      if (more) {
+        // stages issued after stage l + 1: l + 2 … min(l + ns − 1, kLoop − 1)
+        wait_vm_at_most(__builtin_amdgcn_readfirstlane(min(ns - 2, a.kLoop - 2 - l) * ninst));
+        waitcnt_lgkm0();  // this wavefront's reads of slot cur are complete
+        // every wavefront: stage l + 1 landed, done reading slot cur
+        __builtin_amdgcn_s_barrier();
+        if constexpr (NCS >= 2) load_frags(nx, 0, 0);  // the last chunk-step uses slot 1
+      }
+      // last chunk-step; its slots open the window of stage l + ns (into slot cur)
+      const bool load2 = OPEN || l + ns < a.kLoop;
+      StageBase sb2{0, 0, 0};
+      if (load2) sb2 = stage_base(l + ns, cur);
 #pragma unroll
       for (int q = 0; q < TMTN; ++q) {
-        mfma1(cs & 1, q);
-        dma_at(sbs, load, TMTN + cs * TMTN + q);
+        mfma1((NCS - 1) & 1, q);
+        dma_at(sb2, load2, q, open);
       }
-    }
-    const bool more = l + 1 < a.kLoop;
-    const u32x4* nx = lds + ((l + 1) % ns) * stage;
-    if (more) {
-      // stages issued after stage l + 1: l + 2 … min(l + ns − 1, kLoop − 1)
-      wait_vm_at_most(__builtin_amdgcn_readfirstlane(min(ns - 2, a.kLoop - 2 - l) * ninst));
-      waitcnt_lgkm0();  // this wavefront's reads of slot cur are complete
-      // every wavefront: stage l + 1 landed, done reading slot cur
-      __builtin_amdgcn_s_barrier();
-      if constexpr (NCS >= 2) load_frags(nx, 0, 0);  // the last chunk-step uses slot 1
-    }
-    // last chunk-step; its slots open the window of stage l + ns (into slot cur)
-    const bool load2 = l + ns < a.kLoop;
-    StageBase sb2{0, 0, 0};
-    if (load2) sb2 = stage_base(l + ns, cur);
-#pragma unroll
-    for (int q = 0; q < TMTN; ++q) {
-      mfma1((NCS - 1) & 1, q);
-      dma_at(sb2, load2, q);
-    }
-    if constexpr (NCS == 1) {
-      if (more) load_frags(nx, 0, 0);
-    }
-  }
+      if constexpr (NCS == 1) {
+        if (more) load_frags(nx, 0, 0);
+      }
+    };
+    int l = 0;
+    for (; l + ns < a.kLoop; ++l) stage_step(l, std::true_type{});
+    for (; l < a.kLoop; ++l) stage_step(l, std::false_type{});
+  };
+  if (ninst == kMaxDlInst)
+    run(std::integral_constant<int, kMaxDlInst>{});
+  else if (ninst == kMaxDlInst / 2)
+    run(std::integral_constant<int, kMaxDlInst / 2>{});
+  else
+    run(std::integral_constant<int, 0>{});
 
   float* Cw = a.C + static_cast<int64_t>(gm) * BM * a.N + static_cast<int64_t>(gn) * BN;
 #pragma unroll
