@@ -37,21 +37,13 @@ def log(msg):
 
 
 def hand_s0(w):
-    """A hand-crafted start state (§4.2 allows one): 64×64 workgroup tiles of
-    2×2 wavefronts with 32-wide MFMA blocks and a 32-deep K stage."""
-    if w.d == (4, 4, 4):
-        m = (w.M // 64, 2, 1, 32) if w.M >= 64 else (1, 1, 1, w.M)
-        n_odd = w.N // 64
-        n = (n_odd, 2, 1, 32)
-        k = (w.K // 32, 1, 2, 16)
-        return (m, k, n, 32 if w.mfma_coord else 0)
-    if w.d == (3, 3, 3):
-        return ((w.M // 64, 2, 32), (w.K // 32, 2, 16), (w.N // 64, 2, 32), 0)
-    raise ValueError("no hand-crafted start for this level layout")
+    from paper_1909_10616_amd.gemmtune import hand_start
+    return hand_start(w.M, w.N, w.K, w.d, w.mfma_coord)
 
 
 def fmt_cfg(c):
-    return "m{}k{}n{}mfma{}".format(list(c[0]), list(c[1]), list(c[2]), c[3])
+    from paper_1909_10616_amd.gemmtune import fmt_cfg as f
+    return f(c)
 
 
 def kernel_name(w, info):

@@ -193,12 +193,12 @@ typedef struct gt_tune_result {
   uint64_t best_rank;
   double best_cost;      /* cost_min (ms in GPU mode) */
   int64_t timed;         /* configurations timed (≤ budget) */
-  int64_t popped;
+  int64_t popped;        /* G-BFS: queue pops; random search: draws */
   int64_t skipped_illegit;
   int64_t skipped_visited;
   int64_t failed;        /* timed with cost +inf */
   double wall_s;
-  int32_t stop_reason;   /* 0 budget, 1 queue empty, 2 time limit */
+  int32_t stop_reason;   /* 0 budget, 1 queue empty, 2 time limit, 3 draws exhausted */
   int32_t reserved;
 } gt_tune_result;
 
@@ -207,9 +207,25 @@ int gt_tune_opts_init(gt_tune_opts* opts);
 
 /* G-BFS over the space. cost == NULL times gemm_run on the GPU with
  * opts->A/B/C/stream (and checks outputs when opts->check); otherwise
- * cost(cfg, rank, ctx) is called for every timed configuration. */
+ * cost(cfg, rank, ctx) is called for every timed configuration. A candidate
+ * that fails to launch or mismatches is logged with cost +inf and the search
+ * goes on; a device error that outlives the failing call (a kernel fault)
+ * ends the search with GT_EHIP, *out holding the search up to that point and
+ * gt_last_error() naming the configuration that was being timed. */
 int tune_gbfs(const gt_space* sp, const gt_tune_opts* opts, gt_cost_fn cost,
               void* ctx, gt_tune_result* out);
+
+/* Random search at an equal budget, the baseline the paper's tuners are
+ * compared with (§5): ranks drawn uniformly, r = SplitMix64(opts->seed) mod
+ * |ξ|; illegitimate and already-timed draws are skipped without cost; every
+ * other draw is timed (GPU or callback exactly as in tune_gbfs) until
+ * opts->budget configurations are timed, opts->t_max_s elapses, or
+ * 64·budget + 1024 draws were made (stop_reason 3). opts->s0 and opts->rho
+ * are not used (rho must still be ≥ 1). s* is the first minimum cost; with
+ * nothing timed it is the configuration of rank 0 at cost +inf.
+ * Same ownership and error behaviour as tune_gbfs. */
+int tune_random(const gt_space* sp, const gt_tune_opts* opts, gt_cost_fn cost,
+                void* ctx, gt_tune_result* out);
 
 /* Thread-local message of the last failure. */
 const char* gt_last_error(void);

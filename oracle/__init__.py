@@ -87,6 +87,8 @@ def lib():
         L.or_splitmix64_next.restype = u64
         L.or_gbfs.argtypes = [SP, CF, ctypes.c_int, i64, u64, _COST_FN, p,
                               ctypes.POINTER(_GbfsResult), p, p, i64]
+        L.or_random_search.argtypes = [SP, i64, u64, _COST_FN, p, ctypes.POINTER(_GbfsResult),
+                                       p, p, i64]
         _lib = L
     return _lib
 
@@ -267,6 +269,28 @@ def gbfs(space: Space, s0, rho: int, budget: int, seed: int, cost_fn):
                        _ptr(log_c), budget)
     if rc:
         raise ValueError("or_gbfs: bad argument (illegitimate s0, budget < 1 or rho < 1)")
+    n = int(res.timed)
+    return {"best": space._from_c(res.best), "best_cost": float(res.best_cost),
+            "timed": n, "popped": int(res.popped),
+            "log_ranks": [int(v) for v in log_r[:n]], "log_costs": [float(v) for v in log_c[:n]]}
+
+
+def random_search(space: Space, budget: int, seed: int, cost_fn):
+    """Equal-budget random search (§5 baseline): uniform draws by SplitMix64,
+    illegitimate and repeated draws skipped. Same result dict as gbfs();
+    ``popped`` counts the draws."""
+    log_r = np.zeros(budget, dtype=np.uint64)
+    log_c = np.zeros(budget, dtype=np.float64)
+
+    def _cb(cptr, rank, _ctx):
+        return float(cost_fn(space._from_c(cptr.contents), int(rank)))
+
+    cb = _COST_FN(_cb)
+    res = _GbfsResult()
+    rc = lib().or_random_search(ctypes.byref(space._s), int(budget), int(seed), cb, None,
+                                ctypes.byref(res), _ptr(log_r), _ptr(log_c), budget)
+    if rc:
+        raise ValueError("or_random_search: bad argument (budget < 1)")
     n = int(res.timed)
     return {"best": space._from_c(res.best), "best_cost": float(res.best_cost),
             "timed": n, "popped": int(res.popped),

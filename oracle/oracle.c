@@ -529,3 +529,51 @@ int or_gbfs(const or_space* sp, const or_config* s0, int rho, int64_t budget,
   free_tables(&tb);
   return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Random search at an equal budget (§5 baseline).                          */
+/* ------------------------------------------------------------------------ */
+
+int or_random_search(const or_space* sp, int64_t budget, uint64_t seed, or_cost_fn cost,
+                     void* ctx, or_gbfs_result* res, uint64_t* log_ranks, double* log_costs,
+                     int64_t log_cap) {
+  uint64_t size;
+  if (or_space_size(sp, &size) || !cost || !res || budget < 1) return -1;
+  tables tb;
+  build_tables(sp, &tb);
+  unsigned char* vis = (unsigned char*)calloc((size_t)(size / 8 + 1), 1);
+  uint64_t rng = seed;
+  int64_t timed = 0, draws = 0;
+  const int64_t max_draws = 64 * budget + 1024;
+  double cost_min = INFINITY;
+  uint64_t best = 0;
+  int have = 0;
+  while (timed < budget && draws < max_draws) {
+    const uint64_t r = or_splitmix64_next(&rng) % size;
+    ++draws;
+    or_config c;
+    unrank_with(sp, &tb, r, &c);
+    if (!or_legit(sp, &c)) continue;
+    if (vis[r / 8] & (1u << (r % 8))) continue;
+    vis[r / 8] |= (unsigned char)(1u << (r % 8));
+    const double v = cost(&c, r, ctx);
+    if (timed < log_cap) {
+      log_ranks[timed] = r;
+      log_costs[timed] = v;
+    }
+    ++timed;
+    if (!have || v < cost_min) {
+      cost_min = v;
+      best = r;
+      have = 1;
+    }
+  }
+  unrank_with(sp, &tb, best, &res->best);
+  res->best.legit = or_legit(sp, &res->best);
+  res->best_cost = cost_min;
+  res->timed = timed;
+  res->popped = draws;
+  free(vis);
+  free_tables(&tb);
+  return 0;
+}

@@ -86,6 +86,18 @@ int or_gbfs(const or_space* sp, const or_config* s0, int rho, int64_t budget,
             uint64_t seed, or_cost_fn cost, void* ctx, or_gbfs_result* res,
             uint64_t* log_ranks, double* log_costs, int64_t log_cap);
 
+/* Random search at an equal budget (the baseline the paper's tuners are
+ * compared with, §5): ranks are drawn uniformly, r = splitmix64(seed) mod |ξ|;
+ * illegitimate and already-timed draws are skipped (no budget), every other
+ * draw is timed until `budget` configurations have been timed or
+ * 64·budget + 1024 draws were made; the best is the first minimum cost.
+ * res->popped holds the number of draws. Returns 0, or -1 on a bad argument
+ * (budget < 1). When nothing was timed, res->best is the configuration of
+ * rank 0 and res->best_cost is +inf. */
+int or_random_search(const or_space* sp, int64_t budget, uint64_t seed, or_cost_fn cost,
+                     void* ctx, or_gbfs_result* res, uint64_t* log_ranks, double* log_costs,
+                     int64_t log_cap);
+
 #ifdef __cplusplus
 }
 #endif

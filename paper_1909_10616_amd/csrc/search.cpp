@@ -1,11 +1,16 @@
-// Greedy Best-First Search over the configuration space (§4.2, Alg.1).
+// Greedy Best-First Search over the configuration space (§4.2, Alg.1), and
+// the equal-budget random search the paper's tuners are measured against
+// (§5).
 //
-// The queue is ordered by increasing (cost, rank); S_v is a hash set of
-// ranks. Each pop takes ρ neighbours of g(s) by a partial Fisher–Yates
+// G-BFS: the queue is ordered by increasing (cost, rank); S_v is a hash set
+// of ranks. Each pop takes ρ neighbours of g(s) by a partial Fisher–Yates
 // shuffle driven by SplitMix64 (Steele, Lea & Flood 2014), then times every
 // pick that is legitimate and unvisited. A configuration counts toward the
 // budget when it is timed; a failed or mismatching run costs +inf, is
 // counted and visited, and is never pushed.
+//
+// Random search: ranks drawn uniformly (SplitMix64 mod |ξ|), illegitimate
+// and repeated draws skipped without cost, at most 64·budget + 1024 draws.
 #include <hip/hip_runtime.h>
 
 #include <chrono>
@@ -37,7 +42,22 @@ struct GpuCtx {
   void* c_ref;
   double tol;
   hipStream_t s;
+  hipError_t fatal = hipSuccess;  // device error that outlives the failed call
 };
+
+std::string describe(const gt_config& c) {
+  std::string r = "((";
+  auto tup = [&r](const int64_t* v, int d) {
+    for (int i = 0; i < d; ++i) r += (i ? "," : "") + std::to_string(v[i]);
+  };
+  tup(c.m, c.d_m);
+  r += "),(";
+  tup(c.k, c.d_k);
+  r += "),(";
+  tup(c.n, c.d_n);
+  r += ")," + std::to_string(c.mfma) + ")";
+  return r;
+}
 
 // Times one configuration on the GPU; fills the log record; returns the cost.
 double gpu_cost(GpuCtx& g, const gt_config& c, double cost_min, gt_log_entry* rec) {
@@ -51,13 +71,21 @@ double gpu_cost(GpuCtx& g, const gt_config& c, double cost_min, gt_log_entry* re
   rec->first_ms = first;
   rec->rel_err = NAN;
   if (rc != GT_OK) {
+    // A failed launch (no kernel, bad shape) leaves the device usable; a
+    // fault in a kernel does not, and every later call would fail too.
+    const hipError_t e = hipDeviceSynchronize();
+    if (e != hipSuccess) g.fatal = e;
     rec->status = 2;
     rec->cost_ms = INFINITY;
     return INFINITY;
   }
   if (g.o->check) {
     double rel = NAN;
-    if (compare_on_gpu(g.o->C, g.c_ref, g.M * g.N, g.s, &rel) != GT_OK || !(rel <= g.tol)) {
+    if (compare_on_gpu(g.o->C, g.c_ref, g.M * g.N, g.s, &rel) != GT_OK) {
+      const hipError_t e = hipDeviceSynchronize();
+      if (e != hipSuccess) g.fatal = e;
+    }
+    if (g.fatal != hipSuccess || !(rel <= g.tol)) {
       rec->status = 3;
       rec->rel_err = rel;
       rec->cost_ms = INFINITY;
@@ -91,22 +119,132 @@ int gt_tune_opts_init(gt_tune_opts* o) {
   return GT_OK;
 }
 
+}  // extern "C"
+
+namespace gt {
+namespace {
+
+// What both searches share: the space, the timing (callback or GPU, with the
+// reference product computed once), the log and the result counters.
+struct Tuner {
+  Space s;
+  const gt_tune_opts* o = nullptr;
+  gt_cost_fn cost = nullptr;
+  void* ctx = nullptr;
+  gt_tune_result* out = nullptr;
+  GpuCtx g{};
+  void* owned_ref = nullptr;
+  double cost_min = INFINITY;
+  std::chrono::steady_clock::time_point t0 = std::chrono::steady_clock::now();
+
+  ~Tuner() {
+    if (owned_ref) (void)hipFree(owned_ref);
+  }
+
+  int init(const gt_space* sp, const gt_tune_opts* opts, gt_cost_fn cb, void* cb_ctx,
+           gt_tune_result* res, const char* who) {
+    if (int rc = make_space(sp, &s)) return rc;
+    if (!opts || !res) {
+      set_error(std::string(who) + ": null options or result");
+      return GT_EINVAL;
+    }
+    if (opts->budget < 1 || opts->rho < 1) {
+      set_error(std::string(who) + ": budget and rho must be >= 1");
+      return GT_EINVAL;
+    }
+    o = opts;
+    cost = cb;
+    ctx = cb_ctx;
+    out = res;
+    std::memset(out, 0, sizeof(*out));
+    return GT_OK;
+  }
+
+  // GPU mode: operands, tolerance, and the reference product (once).
+  int prepare_gpu(const gt_space* sp, const char* who) {
+    if (cost) return GT_OK;
+    if (!o->A || !o->B || !o->C) {
+      set_error(std::string(who) + ": GPU mode needs A, B and C");
+      return GT_EINVAL;
+    }
+    g.o = o;
+    g.M = sp->M;
+    g.N = sp->N;
+    g.K = sp->K;
+    g.dtype = sp->dtype;
+    g.s = static_cast<hipStream_t>(o->stream);
+    g.tol = sp->dtype == GT_F32 ? 1e-5 * std::sqrt(static_cast<double>(sp->K)) : 2e-3;
+    g.c_ref = o->c_ref;
+    if (o->check) {
+      if (!g.c_ref) {
+        hipError_t e = hipMalloc(&owned_ref, static_cast<size_t>(sp->M * sp->N) * sizeof(float));
+        if (e != hipSuccess) {
+          owned_ref = nullptr;
+          set_error(std::string(who) + ": hipMalloc reference: " + hipGetErrorString(e));
+          return GT_EHIP;
+        }
+        g.c_ref = owned_ref;
+      }
+      int rc = gt_reference_gemm(o->A, o->B, g.c_ref, sp->M, sp->N, sp->K, sp->dtype, o->stream);
+      if (rc == GT_OK && hipStreamSynchronize(g.s) != hipSuccess) rc = GT_EHIP;
+      if (rc != GT_OK) return rc;
+    }
+    return GT_OK;
+  }
+
+  double elapsed() const {
+    return std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+  }
+
+  // Times one configuration, logs it, counts it; returns its cost.
+  double time_one(const gt_config& c, uint64_t rank) {
+    gt_log_entry rec{};
+    rec.rank = rank;
+    double v;
+    if (cost) {
+      v = cost(&c, rank, ctx);
+      rec.cost_ms = v;
+      rec.first_ms = v;
+      rec.rel_err = NAN;
+      rec.status = std::isinf(v) ? 2 : 0;
+    } else {
+      v = gpu_cost(g, c, cost_min, &rec);
+    }
+    if (o->log && out->timed < o->log_cap) o->log[out->timed] = rec;
+    ++out->timed;
+    if (std::isinf(v)) ++out->failed;
+    return v;
+  }
+
+  // After a device error that outlives its call: the result so far, and
+  // GT_EHIP with the configuration that was being timed.
+  bool fatal() const { return g.fatal != hipSuccess; }
+  int fail_fatal(const char* who, const gt_config& c, uint64_t best) {
+    finish(best);
+    set_error(std::string(who) + ": device error while timing " + describe(c) + ": " +
+              hipGetErrorString(g.fatal));
+    return GT_EHIP;
+  }
+
+  void finish(uint64_t best) {
+    unrank_into(s, best, &out->best);
+    out->best_rank = best;
+    out->best_cost = cost_min;
+    out->wall_s = elapsed();
+  }
+};
+
+}  // namespace
+}  // namespace gt
+
+extern "C" {
+
 int tune_gbfs(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn cost, void* ctx,
               gt_tune_result* out) {
   using namespace gt;
-  using clock = std::chrono::steady_clock;
-  const auto t0 = clock::now();
-  Space s;
-  if (int rc = make_space(sp, &s)) return rc;
-  if (!o || !out) {
-    set_error("tune_gbfs: null options or result");
-    return GT_EINVAL;
-  }
-  if (o->budget < 1 || o->rho < 1) {
-    set_error("tune_gbfs: budget and rho must be >= 1");
-    return GT_EINVAL;
-  }
-  std::memset(out, 0, sizeof(*out));
+  Tuner t;
+  if (int rc = t.init(sp, o, cost, ctx, out, "tune_gbfs")) return rc;
+  const Space& s = t.s;
 
   // start state: caller's, or [D,1,...,1] per dimension with MFMA 16
   gt_config s0{};
@@ -132,60 +270,7 @@ int tune_gbfs(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn cost, void* 
     set_error("tune_gbfs: s0 is not legitimate");
     return GT_EILLEGIT;
   }
-
-  GpuCtx g{};
-  void* owned_ref = nullptr;
-  if (!cost) {
-    if (!o->A || !o->B || !o->C) {
-      set_error("tune_gbfs: GPU mode needs A, B and C");
-      return GT_EINVAL;
-    }
-    g.o = o;
-    g.M = sp->M;
-    g.N = sp->N;
-    g.K = sp->K;
-    g.dtype = sp->dtype;
-    g.s = static_cast<hipStream_t>(o->stream);
-    g.tol = sp->dtype == GT_F32 ? 1e-5 * std::sqrt(static_cast<double>(sp->K)) : 2e-3;
-    g.c_ref = o->c_ref;
-    if (o->check) {
-      if (!g.c_ref) {
-        hipError_t e = hipMalloc(&owned_ref, static_cast<size_t>(sp->M * sp->N) * sizeof(float));
-        if (e != hipSuccess) {
-          set_error(std::string("tune_gbfs: hipMalloc reference: ") + hipGetErrorString(e));
-          return GT_EHIP;
-        }
-        g.c_ref = owned_ref;
-      }
-      int rc = gt_reference_gemm(o->A, o->B, g.c_ref, sp->M, sp->N, sp->K, sp->dtype, o->stream);
-      if (rc == GT_OK && hipStreamSynchronize(g.s) != hipSuccess) rc = GT_EHIP;
-      if (rc != GT_OK) {
-        if (owned_ref) (void)hipFree(owned_ref);
-        return rc;
-      }
-    }
-  }
-
-  auto elapsed = [&]() { return std::chrono::duration<double>(clock::now() - t0).count(); };
-  double cost_min = INFINITY;
-  auto time_one = [&](const gt_config& c, uint64_t rank) -> double {
-    gt_log_entry rec{};
-    rec.rank = rank;
-    double v;
-    if (cost) {
-      v = cost(&c, rank, ctx);
-      rec.cost_ms = v;
-      rec.first_ms = v;
-      rec.rel_err = NAN;
-      rec.status = std::isinf(v) ? 2 : 0;
-    } else {
-      v = gpu_cost(g, c, cost_min, &rec);
-    }
-    if (o->log && out->timed < o->log_cap) o->log[out->timed] = rec;
-    ++out->timed;
-    if (std::isinf(v)) ++out->failed;
-    return v;
-  };
+  if (int rc = t.prepare_gpu(sp, "tune_gbfs")) return rc;
 
   using Item = std::pair<double, uint64_t>;  // (cost, rank), smallest first
   std::priority_queue<Item, std::vector<Item>, std::greater<Item>> q;
@@ -193,10 +278,11 @@ int tune_gbfs(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn cost, void* 
   uint64_t rng = o->seed;
 
   const uint64_t r0 = rank_of(s, s0);
-  const double c0 = time_one(s0, r0);
+  const double c0 = t.time_one(s0, r0);
   visited.insert(r0);
-  cost_min = c0;
+  t.cost_min = c0;
   uint64_t best = r0;
+  if (t.fatal()) return t.fail_fatal("tune_gbfs", s0, best);
   if (!std::isinf(c0)) q.push({c0, r0});
 
   out->stop_reason = 1;
@@ -210,7 +296,7 @@ int tune_gbfs(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn cost, void* 
       out->stop_reason = 1;
       break;
     }
-    if (o->t_max_s > 0.0 && elapsed() >= o->t_max_s) {
+    if (o->t_max_s > 0.0 && t.elapsed() >= o->t_max_s) {
       out->stop_reason = 2;
       break;
     }
@@ -235,22 +321,69 @@ int tune_gbfs(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn cost, void* 
         ++out->skipped_visited;
         continue;
       }
-      const double v = time_one(g_s[i], r);
+      const double v = t.time_one(g_s[i], r);
+      if (t.fatal()) return t.fail_fatal("tune_gbfs", g_s[i], best);
       visited.insert(r);
       if (!std::isinf(v)) q.push({v, r});
-      if (v < cost_min) {
-        cost_min = v;
+      if (v < t.cost_min) {
+        t.cost_min = v;
         best = r;
       }
     }
   }
   if (out->timed >= o->budget) out->stop_reason = 0;
+  t.finish(best);
+  return GT_OK;
+}
 
-  unrank_into(s, best, &out->best);
-  out->best_rank = best;
-  out->best_cost = cost_min;
-  out->wall_s = elapsed();
-  if (owned_ref) (void)hipFree(owned_ref);
+int tune_random(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn cost, void* ctx,
+                gt_tune_result* out) {
+  using namespace gt;
+  Tuner t;
+  if (int rc = t.init(sp, o, cost, ctx, out, "tune_random")) return rc;
+  if (int rc = t.prepare_gpu(sp, "tune_random")) return rc;
+  const Space& s = t.s;
+  std::unordered_set<uint64_t> visited;
+  uint64_t rng = o->seed;
+  const int64_t max_draws = 64 * o->budget + 1024;
+  uint64_t best = 0;
+  bool have = false;
+  out->stop_reason = 3;
+  while (true) {
+    if (out->timed >= o->budget) {
+      out->stop_reason = 0;
+      break;
+    }
+    if (out->popped >= max_draws) {
+      out->stop_reason = 3;
+      break;
+    }
+    if (o->t_max_s > 0.0 && t.elapsed() >= o->t_max_s) {
+      out->stop_reason = 2;
+      break;
+    }
+    const uint64_t r = splitmix64(&rng) % s.size;
+    ++out->popped;
+    gt_config c;
+    unrank_into(s, r, &c);
+    if (!c.legit) {
+      ++out->skipped_illegit;
+      continue;
+    }
+    if (visited.count(r)) {
+      ++out->skipped_visited;
+      continue;
+    }
+    visited.insert(r);
+    const double v = t.time_one(c, r);
+    if (t.fatal()) return t.fail_fatal("tune_random", c, best);
+    if (!have || v < t.cost_min) {
+      t.cost_min = v;
+      best = r;
+      have = true;
+    }
+  }
+  t.finish(best);
   return GT_OK;
 }
 

@@ -20,7 +20,7 @@ MAXD = 4
 F32, BF16 = 0, 1
 ADJACENT, ANY_PAIR = 0, 1
 STATUS = {0: "ok", 1: "early-abort", 2: "launch-failure", 3: "mismatch"}
-STOP = {0: "budget", 1: "queue-empty", 2: "time-limit"}
+STOP = {0: "budget", 1: "queue-empty", 2: "time-limit", 3: "draws-exhausted"}
 
 
 class GemmTuneError(RuntimeError):
@@ -80,7 +80,7 @@ class gt_tune_result(ctypes.Structure):
 
 EXPORTS = ("gt_space_size", "enumerate_configs", "config_rank", "config_unrank", "config_legit",
            "neighbours", "gemm_run", "gt_measure", "gt_reference_gemm", "gt_compare",
-           "gt_lower", "gt_tune_opts_init", "tune_gbfs", "gt_last_error")
+           "gt_lower", "gt_tune_opts_init", "tune_gbfs", "tune_random", "gt_last_error")
 
 _lib = None
 
@@ -112,6 +112,8 @@ def lib():
     L.gt_tune_opts_init.argtypes = [ctypes.POINTER(gt_tune_opts)]
     L.tune_gbfs.argtypes = [SP, ctypes.POINTER(gt_tune_opts), gt_cost_fn, P,
                             ctypes.POINTER(gt_tune_result)]
+    L.tune_random.argtypes = [SP, ctypes.POINTER(gt_tune_opts), gt_cost_fn, P,
+                              ctypes.POINTER(gt_tune_result)]
     L.gt_last_error.restype = ctypes.c_char_p
     for name in EXPORTS:
         if name != "gt_last_error":
@@ -283,13 +285,8 @@ def gt_compare(C, R, stream=None) -> float:
     return rel.value
 
 
-def tune_gbfs(space: Space, budget: int, s0=None, rho: int = 5, seed: int = 0, runs: int = 10,
-              warmup: int = 1, check: bool = True, t_max_s: float = 0.0,
-              max_run_ms: float = 250.0, abort_factor: float = 50.0, A=None, B=None, C=None,
-              c_ref=None, cost_fn=None, stream=None) -> dict:
-    """Run G-BFS (Alg.1). With ``cost_fn(cfg, rank) -> float`` the costs are
-    synthetic (no GPU); otherwise A, B, C are GPU tensors and every candidate
-    is timed with ``gemm_run`` on the stream."""
+def _tune(entry, space: Space, budget: int, s0, rho, seed, runs, warmup, check, t_max_s,
+          max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream) -> dict:
     L = lib()
     o = gt_tune_opts()
     _check(L.gt_tune_opts_init(ctypes.byref(o)), "gt_tune_opts_init")
@@ -316,8 +313,8 @@ def tune_gbfs(space: Space, budget: int, s0=None, rho: int = 5, seed: int = 0, r
         o.c_ref = c_ref.data_ptr() if c_ref is not None else None
         o.stream = _stream(stream)
     res = gt_tune_result()
-    _check(L.tune_gbfs(ctypes.byref(space.c), ctypes.byref(o), cb, None, ctypes.byref(res)),
-           "tune_gbfs")
+    _check(getattr(L, entry)(ctypes.byref(space.c), ctypes.byref(o), cb, None, ctypes.byref(res)),
+           entry)
     del keep
     n = int(res.timed)
     entries = [{"rank": int(log[i].rank), "cost_ms": log[i].cost_ms, "first_ms": log[i].first_ms,
@@ -331,6 +328,45 @@ def tune_gbfs(space: Space, budget: int, s0=None, rho: int = 5, seed: int = 0, r
             "log": entries}
 
 
+def tune_gbfs(space: Space, budget: int, s0=None, rho: int = 5, seed: int = 0, runs: int = 10,
+              warmup: int = 1, check: bool = True, t_max_s: float = 0.0,
+              max_run_ms: float = 250.0, abort_factor: float = 50.0, A=None, B=None, C=None,
+              c_ref=None, cost_fn=None, stream=None) -> dict:
+    """Run G-BFS (Alg.1). With ``cost_fn(cfg, rank) -> float`` the costs are
+    synthetic (no GPU); otherwise A, B, C are GPU tensors and every candidate
+    is timed with ``gemm_run`` on the stream."""
+    return _tune("tune_gbfs", space, budget, s0, rho, seed, runs, warmup, check, t_max_s,
+                 max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream)
+
+
+def tune_random(space: Space, budget: int, seed: int = 0, runs: int = 10, warmup: int = 1,
+                check: bool = True, t_max_s: float = 0.0, max_run_ms: float = 250.0,
+                abort_factor: float = 50.0, A=None, B=None, C=None, c_ref=None, cost_fn=None,
+                stream=None) -> dict:
+    """Equal-budget random search (§5 baseline); same timing and result as
+    tune_gbfs, ``popped`` counts the draws."""
+    return _tune("tune_random", space, budget, None, 1, seed, runs, warmup, check, t_max_s,
+                 max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream)
+
+
 def tflops(M, N, K, ms) -> float:
     """2·M·N·K floating-point operations per run (one multiply-add = 2 flops)."""
     return 2.0 * M * N * K / (ms * 1e-3) / 1e12 if ms > 0 and math.isfinite(ms) else 0.0
+
+
+def hand_start(M: int, N: int, K: int, d, mfma_coord: bool):
+    """A hand-crafted start state (§4.2 allows one): 64×64 workgroup tiles of
+    2×2 wavefronts with 32-wide MFMA blocks and a 32-deep K stage, for the
+    level layouts (4, 4, 4) and (3, 3, 3)."""
+    if tuple(d) == (4, 4, 4):
+        m = (M // 64, 2, 1, 32) if M >= 64 else (1, 1, 1, M)
+        n = (N // 64, 2, 1, 32)
+        k = (K // 32, 1, 2, 16)
+        return (m, k, n, 32 if mfma_coord else 0)
+    if tuple(d) == (3, 3, 3):
+        return ((M // 64, 2, 32), (K // 32, 2, 16), (N // 64, 2, 32), 0)
+    raise ValueError("no hand-crafted start for this level layout")
+
+
+def fmt_cfg(c) -> str:
+    return "m{}k{}n{}mfma{}".format(list(c[0]), list(c[1]), list(c[2]), c[3])

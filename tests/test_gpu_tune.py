@@ -68,3 +68,37 @@ def test_gpu_search_is_consistent_and_replays_in_oracle(gt, orc, case):
     assert err <= (1e-5 * K ** 0.5 if dt == "f32" else 2e-3)
     print(f"best {res['best']} {gt.tflops(M, N, K, res['best_cost']):.2f} TFLOP/s after "
           f"{res['timed']} timings in {res['wall_s']:.1f}s", flush=True)
+
+
+RANDOM_CASES = [
+    (256, 256, 256, (3, 3, 3), "f32", False, 48),
+    (512, 512, 512, (4, 4, 4), "bf16", True, 64),
+]
+
+
+@pytest.mark.parametrize("case", RANDOM_CASES, ids=["f32-256", "bf16-512"])
+def test_gpu_random_search_replays_in_oracle(gt, orc, case):
+    """Equal-budget random search on the GPU: the oracle's random search fed
+    the logged costs takes the identical draws and keeps the same s*; every
+    timed output matched the reference; s*'s product matches the oracle."""
+    M, N, K, d, dt, mc, budget = case
+    dev = torch.device("cuda:0")
+    A, B = make_inputs(M, N, K, dt, 1, "uniform" if dt == "f32" else "normal")
+    Ad, Bd = A.to(dev), B.to(dev)
+    C = torch.empty(M, N, device=dev)
+    sp = gt.Space(M, N, K, d, dt, mc)
+    print(f"random search {M}x{N}x{K} {dt} budget {budget}", flush=True)
+    res = gt.tune_random(sp, budget=budget, seed=9, A=Ad, B=Bd, C=C)
+    log = res["log"]
+    assert res["timed"] == len(log) == budget and res["stop_reason"] == "budget"
+    assert all(e["status"] in ("ok", "early-abort") for e in log)
+    os_ = orc.Space(M, N, K, d, dt, mc)
+    table = {e["rank"]: e["cost_ms"] for e in log}
+    rep = orc.random_search(os_, budget, 9, lambda c, r: table.get(r, math.inf))
+    assert rep["log_ranks"] == [e["rank"] for e in log]
+    assert rep["best"] == res["best"] and rep["best_cost"] == res["best_cost"]
+    gt.gemm_run(res["best"], Ad, Bd, C)
+    torch.cuda.synchronize()
+    ref = orc.gemm(raw_bytes(A), raw_bytes(B), M, N, K, dt)
+    err = np.abs(C.cpu().numpy().astype(np.float64) - ref).max() / np.abs(ref).max()
+    assert err <= (1e-5 * K ** 0.5 if dt == "f32" else 2e-3)

@@ -234,3 +234,52 @@ def test_lowering_of_known_configs(gt):
     assert info["grid_y"] == 8 and info["fast"] == 1
     info = gt.lower(((8, 2, 1, 16), (16, 1, 4, 16), (8, 2, 1, 16), 32), 256, 256, 1024, "bf16")
     assert info["fast"] == 0 and info["TM"] == 1
+
+
+RANDOM_CASES = [
+    # (M, N, K, d, dtype, mfma, budget, seed)
+    (256, 256, 256, (3, 3, 3), "f32", False, 64, 0),
+    (1024, 1024, 1024, (4, 4, 4), "f32", False, 200, 5),
+    (4096, 4096, 4096, (4, 4, 4), "bf16", True, 300, 3),
+    (64, 11008, 4096, (4, 4, 4), "bf16", True, 150, 11),
+    (1, 1, 1, (4, 4, 4), "f32", False, 4, 0),
+]
+
+
+@pytest.mark.parametrize("case", RANDOM_CASES, ids=[f"{c[0]}x{c[1]}x{c[2]}-{c[4]}" for c in RANDOM_CASES])
+def test_tune_random_synthetic_trajectory_matches_oracle(gt, orc, case):
+    M, N, K, d, dt, mc, budget, seed = case
+    sp = gt.Space(M, N, K, d, dt, mc)
+    osp = orc.Space(M, N, K, d, dt, mc)
+    cost = lambda c, r: float((r * 2654435761) % 100003) / 7.0   # noqa: E731
+    res = gt.tune_random(sp, budget=budget, seed=seed, cost_fn=cost)
+    ref = orc.random_search(osp, budget, seed, cost)
+    assert [e["rank"] for e in res["log"]] == ref["log_ranks"]
+    assert [e["cost_ms"] for e in res["log"]] == ref["log_costs"]
+    assert res["timed"] == ref["timed"] and res["popped"] == ref["popped"]
+    assert res["best"] == ref["best"] and res["best_cost"] == ref["best_cost"]
+    assert res["skipped_illegit"] + res["skipped_visited"] + res["timed"] == res["popped"]
+    want = "budget" if res["timed"] == budget else "draws-exhausted"
+    assert res["stop_reason"] == want
+
+
+def test_tune_random_errors_and_time_limit(gt):
+    sp = gt.Space(256, 256, 256, (3, 3, 3), "f32", False)
+    with pytest.raises(gt.GemmTuneError):
+        gt.tune_random(sp, budget=0, cost_fn=lambda c, r: 1.0)
+    # GPU mode (no callback) without operands is refused by the C ABI itself
+    lib = gt.lib()
+    o = gt.gt_tune_opts()
+    assert lib.gt_tune_opts_init(ctypes.byref(o)) == 0
+    res = gt.gt_tune_result()
+    rc = lib.tune_random(ctypes.byref(sp.c), ctypes.byref(o), gt.gt_cost_fn(), None, ctypes.byref(res))
+    assert rc == -1 and b"A, B and C" in lib.gt_last_error()
+    ls = gt.Space(1024, 1024, 1024, (4, 4, 4), "f32", False)
+    import time
+
+    def slow(cfg, rank):
+        time.sleep(0.01)
+        return 1.0
+
+    r = gt.tune_random(ls, budget=10 ** 6, t_max_s=0.2, cost_fn=slow)
+    assert r["stop_reason"] == "time-limit" and 1 <= r["timed"] < 200
