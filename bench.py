@@ -4,10 +4,12 @@ A step is one pass of the whole path on the resident synthetic inputs: a
 G-BFS search (§4.2 Alg.1) over the tiling space with its budget of timed
 configurations — enumeration/rank, legitimacy, neighbours, ρ-sampling,
 lowering, every candidate GEMM run and timed on the GPU and checked against
-the reference — followed by the report: the best configuration s* re-timed
-over REPEAT back-to-back launches between HIP events on the bench stream.
+the reference — followed by the report: s* and the next TOPK − 1 configurations of
+the search log by cost, each re-timed over REPEAT back-to-back launches
+between HIP events on the bench stream; the fastest is reported.
 
-value   = TFLOP/s of s* (2·M·N·K per run) from that re-timing;
+value   = TFLOP/s of the reported configuration (2·M·N·K per run) from its
+          re-timing;
 ms_per_step = wall time of one step (search + report).
 
 Prints ONE JSON line (rank 0). Only one GPU: --gpus above 1 exits.
@@ -30,6 +32,7 @@ METRIC = "best-found GEMM TFLOP/s (% of MFMA peak); configs timed / % of space"
 PEAK = {"bf16": 2516.6, "f32": 157.3}
 HBM_GBS = 8000.0
 REPEAT = 200
+TOPK = 4
 
 
 def log(msg):
@@ -191,18 +194,33 @@ def main():
                           "lds_bytes": info["lds_bytes"]}))
         return
 
+    def retime(cfg):
+        gt.gemm_run(cfg, Ad, Bd, C, stream=stream)   # warm the kernel
+        ev0.record(stream)
+        for _ in range(REPEAT):
+            gt.gemm_run(cfg, Ad, Bd, C, stream=stream)
+        ev1.record(stream)
+        ev1.synchronize()
+        return ev0.elapsed_time(ev1) / REPEAT
+
     def step():
         with torch.cuda.stream(stream):
             res = gt.tune_gbfs(sp, budget=budget, s0=s0, rho=args.rho, seed=args.seed,
                                A=Ad, B=Bd, C=C, c_ref=Cref, stream=stream)
-            best = res["best"]
-            gt.gemm_run(best, Ad, Bd, C, stream=stream)   # warm the chosen kernel
-            ev0.record(stream)
-            for _ in range(REPEAT):
-                gt.gemm_run(best, Ad, Bd, C, stream=stream)
-            ev1.record(stream)
-            ev1.synchronize()
-        res["best_ms"] = ev0.elapsed_time(ev1) / REPEAT
+            # report: the TOPK configurations of the log with the lowest
+            # (10-run) costs are re-timed over REPEAT launches each, s* first;
+            # the fastest re-timing is the reported configuration
+            ok = sorted((e["cost_ms"], e["rank"]) for e in res["log"] if e["status"] == "ok")
+            ranks = [res["best_rank"]] + [r for _, r in ok if r != res["best_rank"]][:TOPK - 1]
+            top = []
+            for r in ranks:
+                cfg = sp.unrank(r)
+                top.append((retime(cfg), r, cfg))
+            best_ms, best_rank, best = min(top)
+            gt.gemm_run(best, Ad, Bd, C, stream=stream)   # C of the reported configuration
+        res["search_best"], res["search_best_rank"] = res["best"], res["best_rank"]
+        res["best"], res["best_rank"], res["best_ms"] = best, best_rank, best_ms
+        res["top"] = [(fmt_cfg(c), round(ms * 1e3, 2)) for ms, _, c in top]
         return res
 
     for i in range(args.warmup):
@@ -255,7 +273,9 @@ def main():
             "fraction_of_space_pct": 100.0 * last["timed"] / size,
             "best_config": fmt_cfg(last["best"]), "best_rank": last["best_rank"],
             "pct_of_peak": round(100.0 * value / peak, 2),
+            "search_best_config": fmt_cfg(last["search_best"]),
             "search_best_cost_ms": last["best_cost"], "best_ms": best_ms,
+            "retimed_top_us": last["top"],
             "search_wall_s": round(last["wall_s"], 2), "failed": last["failed"],
             "stop": last["stop_reason"], "best_rel_diff_vs_reference": rel,
             "kernel": {k: info[k] for k in ("I", "TM", "TN", "fast", "dl", "ring", "waves", "BM",
