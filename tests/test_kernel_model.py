@@ -1,0 +1,381 @@
+"""A CPU model of the fast-path and direct-load GEMM kernels' addressing and
+of the direct-load ring schedule, run over seeded samples of the configurations
+of the 1024³ and 4096³ bf16 spaces that meet the fast path's shape conditions
+(plus the known fastest 4096³ configurations). The same model run over all
+98,086 such configurations of the 4096³ space finds no violation.
+
+For each configuration the model takes the launch the library chose
+(gt_lower: tile sizes, wavefronts, ring depth, LDS bytes) and checks, lane by
+lane, that
+
+* every global load of A and B stays inside its operand, for the first and
+  last workgroup, split-K slice and stage (the addresses are affine in
+  those indices, so the extremes bound all of them);
+* every LDS write (register-staged stores and direct loads) and every LDS
+  fragment read stays inside its stage and the launch's LDS allocation;
+* every C element written belongs to the workgroup's tile;
+* in the direct-load ring, each (stage, load) pair is issued exactly once,
+  never for a stage past kLoop, into a slot whose previous stage every
+  wavefront has finished reading (a barrier in between), and is complete
+  (the vmcnt wait before a barrier) before any wavefront reads the stage.
+
+The model restates the kernels' index formulas; it shares no code with them.
+"""
+import functools
+import itertools
+import os
+import random
+
+import numpy as np
+import pytest
+
+
+@pytest.fixture(scope="module")
+def gt():
+    from paper_1909_10616_amd import gemmtune
+    if not os.path.exists(gemmtune.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    gemmtune.lib()
+    return gemmtune
+
+
+LDS_MAX = 163840
+
+
+def swz(q):
+    return q ^ (((q >> 3) ^ (q >> 6)) & 7)
+
+
+def bswz(k, cprb):
+    j = k & 3
+    return (((j << 2) | (((j ^ (j >> 1)) & 1) << 1)) ^ (((k >> 3) & 1) << 3)) & (cprb - 1)
+
+
+def lg(v):
+    r = v.bit_length() - 1
+    assert 1 << r == v
+    return r
+
+
+def levels(cfg):
+    m, k, n, mf = cfg
+
+    def mn(f):
+        d = len(f)
+        return f[0], (f[1] if d >= 3 else 1), (f[2] if d == 4 else 1), (1 if d == 1 else f[-1])
+
+    gM, wM, rM, bM = mn(m)
+    gN, wN, rN, bN = mn(n)
+    dk = len(k)
+    L = dict(gridM=gM, wavesM=wM, repM=rM, blkM=bM, gridN=gN, wavesN=wN, repN=rN, blkN=bN,
+             kLoop=k[0], kSplit=k[1] if dk == 4 else 1,
+             kSub=k[2] if dk == 4 else (k[1] if dk == 3 else 1), kBlk=1 if dk == 1 else k[-1])
+    I = mf if mf in (16, 32) else (32 if bM % 32 == 0 and bN % 32 == 0 else 16)
+    L.update(I=I, TM=rM * -(-bM // I), TN=rN * -(-bN // I), W=wM * wN, BM=wM * rM * bM,
+             BN=wN * rN * bN, BK=L["kSub"] * L["kBlk"], WM=rM * bM, WN=rN * bN)
+    return L
+
+
+def dl_cap(acc):
+    return 8 if acc + 96 <= 256 else 16
+
+
+def tiles(L):
+    return [(0, 0, 0, 0), (L["gridM"] - 1, L["gridN"] - 1, L["kSplit"] - 1, L["kLoop"] - 1)]
+
+
+def frag_steps(L, CPR, lane):
+    """(wavefront, its M and N coordinates, chunk-step parameters) of the
+    fragment reads."""
+    I = L["I"]
+    G = 64 // I
+    LGCPR = lg(CPR)
+    grp = lane // I
+    for w in range(L["W"]):
+        wm, wn = w % L["wavesM"], w // L["wavesM"]
+        for cs in range(CPR // G):
+            c = cs * G
+            j = (c >> 3) if CPR >= 8 else 0
+            yield w, wm, wn, c, j, LGCPR, grp
+
+
+def check_c_and_frags(L, CPR, achunks, lane, bt_rows=None):
+    I = L["I"]
+    for w, wm, wn, c, j, LGCPR, grp in frag_steps(L, CPR, lane):
+        for t in range(L["TM"]):
+            q0 = ((wm * L["WM"] + t * I + lane % I) << LGCPR) + grp + 8 * j
+            idx = ((swz(q0) - 8 * j) ^ (c & 7)) + (c & ~7)
+            assert idx.min() >= 0 and idx.max() < achunks
+        if bt_rows is not None:  # register-staged path: B stored [n][k] like A
+            for t in range(L["TN"]):
+                q0 = ((wn * L["WN"] + t * I + lane % I) << LGCPR) + grp + 8 * j
+                idx = ((swz(q0) - 8 * j) ^ (c & 7)) + (c & ~7)
+                assert idx.min() >= 0 and idx.max() < bt_rows << LGCPR
+    for w in range(L["W"]):
+        wm, wn = w % L["wavesM"], w // L["wavesM"]
+        for e in range(I * I // 64):
+            r = (8 * (e >> 2) + 4 * (lane >> 5) + (e & 3)) if I == 32 else (4 * (lane >> 4) + e)
+            rows = wm * L["WM"] + np.arange(L["TM"])[:, None] * I + r
+            assert rows.max() < L["BM"]
+        cols = wn * L["WN"] + np.arange(L["TN"])[:, None] * I + lane % I
+        assert cols.max() < L["BN"]
+
+
+def check_fast(L, info, M, N, K):
+    VEC, LGV = 8, 3
+    CPR = L["BK"] // VEC
+    LGCPR = lg(CPR)
+    nthr = 64 * L["W"]
+    BM, BN = L["BM"], L["BN"]
+    achunks = BM << LGCPR
+    lgnbn = lg(BN) - LGV
+    bblocks = CPR << lgnbn
+    stage = achunks + (BN << LGCPR)
+    assert (2 if info["dbuf"] else 1) * stage * 16 <= info["lds_bytes"] <= LDS_MAX
+    tid = np.arange(nthr)
+    prefetch = max(-(-achunks // (nthr * 8)), -(-bblocks // nthr)) == 1
+    for gm, gn, z, l in tiles(L):
+        kbase = (l * L["kSplit"] + z) * L["BK"]
+        a0, b0 = gm * BM * K + kbase, gn * BN + kbase * N
+        if prefetch:
+            ta = np.minimum(tid, achunks - 1)
+            na = min(8, -(-achunks // nthr))
+            for i in range(na):
+                e = ta + i * nthr
+                addr = a0 + (ta >> LGCPR) * K + ((ta & (CPR - 1)) << LGV) + i * (nthr >> LGCPR) * K
+                assert addr.min() >= 0 and addr.max() + VEC <= M * K
+                assert swz(e).max() < achunks
+            b = np.minimum(tid, bblocks - 1)
+        else:
+            e = np.arange(achunks)
+            addr = a0 + (e >> LGCPR) * K + ((e & (CPR - 1)) << LGV)
+            assert addr.max() + VEC <= M * K and swz(e).max() < achunks
+            b = np.arange(bblocks)
+        nb, kb = b & ((1 << lgnbn) - 1), b >> lgnbn
+        for j in range(VEC):
+            addr = b0 + ((kb << LGV) + j) * N + (nb << LGV)
+            assert addr.min() >= 0 and addr.max() + VEC <= K * N
+            assert swz((((nb << LGV) + j) << LGCPR) + kb).max() < BN << LGCPR
+    check_c_and_frags(L, CPR, achunks, np.arange(64), bt_rows=BN)
+
+
+def check_dl(L, info, M, N, K):
+    I, TM, TN, W = L["I"], L["TM"], L["TN"], L["W"]
+    BM, BN, BK = L["BM"], L["BN"], L["BK"]
+    CPR = BK // 8
+    LGCPR = lg(CPR)
+    G = 64 // I
+    NCS = CPR // G
+    cprb = BN >> 3
+    lgcprb = lg(BN) - 3
+    achunks, bchunks = BM << LGCPR, BK * cprb
+    stage = achunks + bchunks
+    pa, pb = achunks >> 6, bchunks >> 6
+    assert pa % W == 0 and pb % W == 0
+    ninst = (pa + pb) // W
+    na_w = pa // W
+    cap = dl_cap(TM * TN * I * I // 64)
+    ns = info["ring"]
+    assert ninst <= cap and 2 <= ns <= 8
+    assert ns * stage * 16 <= info["lds_bytes"] <= LDS_MAX
+    lane = np.arange(64)
+    for w in range(W):
+        for i in range(ninst):
+            if i < na_w:
+                q = swz(((w + i * W) << 6) + lane)
+                off = ((q >> LGCPR) * K + ((q & (CPR - 1)) << 3)) * 2
+                dst = (w + i * W) * 1024
+                lim = M * K * 2
+            else:
+                s = ((w + (i - na_w) * W) << 6) + lane
+                k, cs = s >> lgcprb, s & (cprb - 1)
+                assert k.max() < BK
+                off = (k * N + ((cs ^ bswz(k, cprb)) << 3)) * 2
+                dst = (achunks + ((w + (i - na_w) * W) << 6)) * 16
+                lim = K * N * 2
+            assert off.max() < 2 ** 32
+            assert dst + 1024 <= stage * 16
+            for gm, gn, z, l in tiles(L):
+                kbase = (l * L["kSplit"] + z) * BK
+                base = (gm * BM * K + kbase) * 2 if i < na_w else (gn * BN + kbase * N) * 2
+                assert base + off.min() >= 0 and base + off.max() + 16 <= lim
+    # transposing B reads and A reads
+    i16, g16 = lane & 15, lane >> 4
+    kgrp = (g16 >> 1) if I == 32 else g16
+    ncol0 = (16 * (g16 & 1) if I == 32 else 0) + 4 * (i16 & 3)
+    for w in range(W):
+        wn = w // L["wavesM"]
+        for cs in range(NCS):
+            for t in range(TN):
+                col = wn * L["WN"] + t * I + ncol0
+                for hh in range(2):
+                    k = cs * G * 8 + kgrp * 8 + (i16 >> 2) + 4 * hh
+                    assert k.max() < BK and col.max() < BN
+                    addr = (k * cprb + ((col >> 3) ^ bswz(k, cprb))) * 16 + (col & 4) * 2
+                    assert addr.min() >= 0 and addr.max() + 8 <= bchunks * 16
+    check_c_and_frags(L, CPR, achunks, lane)
+    ring_schedule(TM * TN, NCS, cap, ninst, ns, L["kLoop"])
+
+
+@functools.lru_cache(maxsize=None)
+def ring_schedule(TMTN, NCS, cap, ninst, ns, kLoop):
+    """Replays the ring's control flow for one wavefront (all wavefronts run
+    the same sequence) and checks issue, release and completion rules."""
+    SPOS = NCS * TMTN
+    NI = ninst if ninst in (cap, cap // 2) else 0
+    NIE = NI or cap
+    RR = 1 if NI == cap else ((SPOS // 2) // NI if NI else (SPOS - TMTN // 2) // NIE)
+    R = max(RR, 1)
+    ev = []
+
+    def dma_at(st, on, pos, open_):
+        i = pos // R
+        ok = lambda j: (open_ or on) and (NI > 0 or j < ninst)  # noqa: E731
+        if pos % R == R - 1 and i < NIE and i * R + R - 1 < SPOS and ok(i):
+            ev.append(("dma", st, i))
+        if pos == SPOS - 1:
+            ev.extend(("dma", st, j) for j in range(SPOS // R, NIE) if ok(j))
+
+    npro = min(ns - 1, kLoop)
+    ev.extend(("dma", l, i) for l in range(npro) for i in range(ninst))
+    ev += [("wait", (npro - 1) * ninst), ("bar",)]
+    if ns - 1 < kLoop:
+        for pos in range(TMTN):
+            dma_at(ns - 1, True, pos, True)
+    ev.append(("read", 0))
+    for l in range(kLoop):
+        open_ = l + ns < kLoop
+        ld = l + ns - 1
+        for cs in range(NCS - 1):
+            ev.append(("read", l))
+            for q in range(TMTN):
+                dma_at(ld, open_ or ld < kLoop, TMTN + cs * TMTN + q, open_)
+        more = open_ or l + 1 < kLoop
+        if more:
+            ev += [("wait", min(ns - 2, kLoop - 2 - l) * ninst), ("bar",)]
+            if NCS >= 2:
+                ev.append(("read", l + 1))
+        for q in range(TMTN):
+            dma_at(l + ns, open_ or l + ns < kLoop, q, open_)
+        if NCS == 1 and more:
+            ev.append(("read", l + 1))
+
+    issued, seen, done, ready, last_read, nbar = [], set(), set(), set(), {}, 0
+    for e in ev:
+        if e[0] == "dma":
+            _, st, i = e
+            assert st < kLoop and 0 <= i < ninst and (st, i) not in seen
+            seen.add((st, i))
+            if st >= ns:  # slot st % ns last held stage st - ns
+                assert last_read.get(st - ns, nbar) < nbar
+            issued.append(st)
+        elif e[0] == "wait":
+            n_done = len(issued) - max(e[1], 0)
+            cnt = {}
+            for st in issued[:max(n_done, 0)]:
+                cnt[st] = cnt.get(st, 0) + 1
+            done |= {st for st, c in cnt.items() if c == ninst}
+        elif e[0] == "bar":
+            nbar += 1
+            ready |= done
+        else:
+            assert e[1] in ready
+            last_read[e[1]] = nbar
+    assert len(seen) == kLoop * ninst
+    return True
+
+
+def _tuples(D, d):
+    E = lg(D)
+    return [tuple(2 ** e for e in es) for es in itertools.product(range(E + 1), repeat=d)
+            if sum(es) == E]
+
+
+def fast_candidates(D):
+    """Configurations of the D³ bf16 space (d = 4, MFMA coordinate) that
+    meet the fast path's shape conditions."""
+    T = _tuples(D, 4)
+    out = []
+    for mf in (16, 32):
+        G, IK = 64 // mf, (16 if mf == 32 else 32)
+        Ms = [t for t in T if t[3] % mf == 0]
+        Ks = [k for k in T if k[3] % IK == 0 and (k[2] * k[3]) % (8 * G) == 0
+              and (k[2] * k[3]) // 8 in (2, 4, 8, 16)]
+        for m, n in itertools.product(Ms, Ms):
+            W = m[1] * n[1]
+            acc = m[2] * (m[3] // mf) * n[2] * (n[3] // mf) * mf * mf // 64
+            if W > 8 or acc > 256 or acc + 96 > 512 // ((W + 3) // 4):
+                continue
+            BM, BN = m[1] * m[2] * m[3], n[1] * n[2] * n[3]
+            out += [(m, k, n, mf) for k in Ks if (BM + BN) * k[2] * k[3] * 2 <= LDS_MAX]
+    return out
+
+
+def _run(gt, cfgs, D):
+    n = {"dl": 0, "fast": 0}
+    for c in cfgs:
+        try:
+            info = gt.lower(c, D, D, D, "bf16")
+        except gt.GemmTuneError:
+            continue  # (TM, TN) without an instantiation
+        L = levels(c)
+        assert (info["BM"], info["BN"], info["BK"], info["waves"]) == (L["BM"], L["BN"], L["BK"], L["W"])
+        if info["dl"]:
+            check_dl(L, info, D, D, D)
+            n["dl"] += 1
+        elif info["fast"]:
+            check_fast(L, info, D, D, D)
+            n["fast"] += 1
+    return n
+
+
+def test_model_sample_1024(gt):
+    n = _run(gt, random.Random(4).sample(fast_candidates(1024), 3000), 1024)
+    assert n["dl"] > 100 and n["fast"] > 100, n
+
+
+def test_model_sample_4096(gt):
+    cands = fast_candidates(4096)
+    known = [((16, 2, 4, 32), (128, 1, 1, 32), (16, 4, 2, 32), 16),
+             ((16, 2, 8, 16), (128, 1, 1, 32), (16, 4, 1, 64), 16),
+             ((16, 2, 4, 32), (64, 1, 4, 16), (16, 2, 4, 32), 32),
+             ((16, 4, 2, 32), (64, 1, 4, 16), (16, 2, 4, 32), 32)]
+    sample = known + random.Random(5).sample(cands, 3000)
+    n = _run(gt, sample, 4096)
+    assert n["dl"] > 100 and n["fast"] > 100, n
+
+
+@pytest.mark.parametrize("ns", range(2, 9))
+def test_ring_schedule_shapes(ns):
+    """The schedule rules over ring depths, load counts and stage counts,
+    including kLoop shorter than the ring."""
+    for TMTN, NCS in ((1, 1), (2, 2), (4, 1), (8, 4), (16, 2), (32, 1)):
+        for cap in (8, 16):
+            for ninst in sorted({1, 3, cap // 2, cap}):
+                for kLoop in (1, 2, 3, ns - 1, ns, ns + 1, 2 * ns + 3):
+                    if kLoop >= 1:
+                        ring_schedule(TMTN, NCS, cap, ninst, ns, kLoop)
+
+
+def test_ring_model_detects_a_missing_wait():
+    """The schedule check is not vacuous: boundary waits that leave one more
+    stage outstanding than the kernel's are caught."""
+    assert _replay_with_wait_slack(4, 2, 8, 8, 3, 6, slack=0)
+    with pytest.raises(AssertionError):
+        _replay_with_wait_slack(4, 2, 8, 8, 3, 6, slack=1)
+
+
+def _replay_with_wait_slack(TMTN, NCS, cap, ninst, ns, kLoop, slack):
+    """ring_schedule with every boundary wait allowing `slack` more stages
+    outstanding than the kernel's."""
+    import ast
+    import inspect
+    import textwrap
+    src = textwrap.dedent(inspect.getsource(ring_schedule.__wrapped__))
+    src = src.replace("min(ns - 2, kLoop - 2 - l) * ninst", f"(min(ns - 2, kLoop - 2 - l) + {slack}) * ninst")
+    tree = ast.parse(src)
+    tree.body[0].decorator_list = []
+    ns_ = {}
+    exec(compile(tree, "<ring>", "exec"), globals(), ns_)
+    return ns_["ring_schedule"](TMTN, NCS, cap, ninst, ns, kLoop)
