@@ -24,6 +24,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -114,6 +116,49 @@ def cpu_baseline(w, A, B, target_s: float):
                       f"{dt:.1f} s"}
 
 
+def library_enumeration(sp):
+    """The library's full enumeration of the space with J (a1, a2), streamed
+    in chunks through enumerate_configs."""
+    from paper_1909_10616_amd import gemmtune as gt
+    chunk = 4_000_000
+    buf = (gt.gt_config * chunk)()
+    n = ctypes.c_uint64()
+    size, legit = sp.size(), 0
+    off = gt.gt_config.legit.offset
+    t = time.perf_counter()
+    for start in range(0, size, chunk):
+        gt._check(gt.lib().enumerate_configs(ctypes.byref(sp.c), start, buf, chunk, ctypes.byref(n)),
+                  "enumerate_configs")
+        raw = np.frombuffer(buf, dtype=np.uint8).reshape(chunk, ctypes.sizeof(gt.gt_config))
+        legit += int(raw[:n.value, off:off + 4].copy().view(np.int32).sum())
+    return {"configs": size, "legitimate": legit, "seconds": round(time.perf_counter() - t, 2)}
+
+
+def oracle_side(w, mode, s0, res, rho, seed):
+    """The oracle's other two host steps on the same workload: the full
+    enumeration of the space with J (a1, a2), and Alg.1 fed the costs the GPU
+    search logged (a3, a4, a8), which must retrace the GPU search exactly."""
+    import oracle
+    osp = oracle.Space(w.M, w.N, w.K, w.d, w.dtype, w.mfma_coord,
+                       mode=oracle.ADJACENT if mode == "adjacent" else oracle.ANY_PAIR)
+    size = osp.size()
+    t = time.perf_counter()
+    legit, chunk = 0, 2_000_000
+    for start in range(0, size, chunk):
+        raw = osp.enumerate_raw(start, min(chunk, size - start))
+        legit += int(raw[:, 100:104].copy().view(np.int32).sum())
+    t_enum = time.perf_counter() - t
+    table = {e["rank"]: e["cost_ms"] for e in res["log"]}
+    t = time.perf_counter()
+    rep = oracle.gbfs(osp, s0, rho, len(res["log"]), seed, lambda c, r: table.get(r, math.inf))
+    t_rep = time.perf_counter() - t
+    return {"enumeration": {"configs": size, "legitimate": legit, "seconds": round(t_enum, 2),
+                            "threads": 1},
+            "gbfs_replay": {"seconds": round(t_rep, 3),
+                            "same_trajectory": rep["log_ranks"] == [e["rank"] for e in res["log"]],
+                            "same_best": rep["best"] == res["search_best"]}}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
@@ -125,6 +170,8 @@ def main():
     ap.add_argument("--rho", type=int, default=5)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--mode", choices=["adjacent", "any"], default="adjacent")
+    ap.add_argument("--no-enumeration", action="store_true",
+                    help="skip the timed full enumeration of the space")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--log-out", default=None, help="write the search log (JSON) here")
@@ -290,12 +337,17 @@ def main():
             "hbm_gbs_at_algorithmic_bytes": round(alg_bytes / (best_ms * 1e-3) / 1e9, 1),
         },
     }
+    if not args.no_enumeration:
+        log("library enumeration of the space ...")
+        out["library_enumeration"] = library_enumeration(sp)
     if args.log_out:
         with open(args.log_out, "w") as f:
             json.dump({"config": out["config"], "log": last["log"]}, f)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         out["cpu_baseline"] = cpu_baseline(w, A, B, args.cpu_seconds)
+        log("oracle enumeration and G-BFS replay ...")
+        out["cpu_baseline"].update(oracle_side(w, args.mode, s0, last, args.rho, args.seed))
     print(json.dumps(out), flush=True)
 
 

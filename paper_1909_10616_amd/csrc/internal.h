@@ -32,6 +32,8 @@ bool is_member(const Space& s, const gt_config& c);
 uint64_t rank_of(const Space& s, const gt_config& c);  // requires is_member
 void unrank_into(const Space& s, uint64_t rank, gt_config* c);
 int legit_of(const Space& s, const gt_config& c);
+// Ranks [start, start + n) (within the space) into out[0 .. n), J filled.
+void enumerate_range(const Space& s, uint64_t start, uint64_t n, gt_config* out);
 // g(s) in ascending rank with J filled; returns the count (≤ kMaxNeighbours).
 constexpr int kMaxNeighbours = 3 * GT_MAXD * (GT_MAXD - 1) + 1;
 int neighbour_list(const Space& s, const gt_config& c, gt_config* out);

@@ -8,6 +8,8 @@
 #include <algorithm>
 #include <cstring>
 #include <mutex>
+#include <thread>
+#include <vector>
 
 #include "internal.h"
 
@@ -212,10 +214,9 @@ void levels_of(const gt_config& c, int dtype, Levels* L) {
   L->elem = dtype == GT_BF16 ? 2 : 4;
 }
 
-int legit_of(const Space& s, const gt_config& c) {
-  if (!is_member(s, c)) return 0;
-  Levels L;
-  levels_of(c, s.dtype, &L);
+namespace {
+// The hardware clauses of J (a member's levels).
+int legit_levels(const Levels& L) {
   if (L.W > 16) return 0;
   if (L.acc > 256) return 0;
   const int64_t simd_share = (L.W + 3) / 4;
@@ -225,6 +226,71 @@ int legit_of(const Space& s, const gt_config& c) {
   if (L.gridM * L.gridN * 64 * L.W > int64_t{4294967295}) return 0;
   if (L.kSplit > 65535) return 0;
   return 1;
+}
+}  // namespace
+
+int legit_of(const Space& s, const gt_config& c) {
+  if (!is_member(s, c)) return 0;
+  Levels L;
+  levels_of(c, s.dtype, &L);
+  return legit_levels(L);
+}
+
+// Configurations of ranks [start, start + n) in canonical order: each
+// dimension's tuples are unranked once into a table, then an odometer over
+// (m, k, n, mfma) fills the records; J from the levels (members by
+// construction). Large requests are split over threads.
+void enumerate_range(const Space& s, uint64_t start, uint64_t n, gt_config* out) {
+  std::vector<int64_t> tab[3];
+  for (int x = 0; x < 3; ++x) {
+    tab[x].resize(s.dim[x].count * GT_MAXD);
+    for (uint64_t r = 0; r < s.dim[x].count; ++r) dim_unrank(s.dim[x], r, &tab[x][r * GT_MAXD]);
+  }
+  auto part = [&](uint64_t first, uint64_t count) {
+    uint64_t rank = first;
+    uint64_t im = rank % s.n_mfma;
+    rank /= s.n_mfma;
+    uint64_t r[3];
+    for (int x = 2; x >= 0; --x) {
+      r[x] = rank % s.dim[x].count;
+      rank /= s.dim[x].count;
+    }
+    gt_config c;
+    std::memset(&c, 0, sizeof(c));
+    c.d_m = s.dim[0].d;
+    c.d_k = s.dim[1].d;
+    c.d_n = s.dim[2].d;
+    Levels L;
+    for (uint64_t i = 0; i < count; ++i) {
+      for (int x = 0; x < 3; ++x)
+        std::memcpy(dim_factors(c, x), &tab[x][r[x] * GT_MAXD], GT_MAXD * sizeof(int64_t));
+      c.mfma = s.mfma_coord ? (im ? 32 : 16) : 0;
+      levels_of(c, s.dtype, &L);
+      c.legit = legit_levels(L);
+      out[first - start + i] = c;
+      if (++im < s.n_mfma) continue;
+      im = 0;
+      for (int x = 2; x >= 0; --x) {
+        if (++r[x] < s.dim[x].count) break;
+        r[x] = 0;
+      }
+    }
+  };
+  const uint64_t per = uint64_t{1} << 20;
+  const unsigned hw = std::max(1u, std::thread::hardware_concurrency());
+  const unsigned nt = static_cast<unsigned>(std::min<uint64_t>(std::min(hw, 16u), (n + per - 1) / per));
+  if (nt <= 1) {
+    part(start, n);
+    return;
+  }
+  std::vector<std::thread> th;
+  const uint64_t chunk = (n + nt - 1) / nt;
+  for (unsigned t = 0; t < nt; ++t) {
+    const uint64_t a = t * chunk;
+    if (a >= n) break;
+    th.emplace_back(part, start + a, std::min(chunk, n - a));
+  }
+  for (auto& t : th) t.join();
 }
 
 int neighbour_list(const Space& s, const gt_config& c, gt_config* out) {
@@ -298,7 +364,7 @@ int enumerate_configs(const gt_space* sp, uint64_t start_rank, gt_config* out, u
     return GT_EINVAL;
   }
   const uint64_t n = std::min<uint64_t>(cap, s.size - start_rank);
-  for (uint64_t i = 0; i < n; ++i) gt::unrank_into(s, start_rank + i, &out[i]);
+  if (n) gt::enumerate_range(s, start_rank, n, out);
   *n_out = n;
   return GT_OK;
 }
