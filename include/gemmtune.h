@@ -40,6 +40,13 @@ typedef enum {
 } gt_status;
 
 typedef enum { GT_F32 = 0, GT_BF16 = 1 } gt_dtype;
+
+/* Operand-layout flag OR-ed into every `dtype` argument (and gt_space.dtype):
+ * A is passed as W = Aᵀ, a K×M row-major array (element (m, k) at
+ * A[k·M + m]), so that the product is C = WᵀB — the perceptron layer
+ * Y = WᵀX of §5 with W ∈ R^(k×m), X ∈ R^(k×n). Without the flag A is M×K
+ * row-major. B and C are unaffected. */
+#define GT_A_KMAJOR 16
 typedef enum { GT_ADJACENT = 0, GT_ANY_PAIR = 1 } gt_neighbour_mode;
 
 /* Configuration space ξ = ξ_m × ξ_k × ξ_n (§3.3 Eq.1–4).
@@ -51,7 +58,7 @@ typedef enum { GT_ADJACENT = 0, GT_ANY_PAIR = 1 } gt_neighbour_mode;
 typedef struct gt_space {
   int64_t M, N, K;
   int32_t d_m, d_k, d_n;   /* 1..GT_MAXD */
-  int32_t dtype;           /* gt_dtype of A and B; C is always fp32 */
+  int32_t dtype;           /* gt_dtype of A and B (| GT_A_KMAJOR); C is fp32 */
   int32_t mfma_coord;      /* 0 or 1 */
   int32_t neighbour_mode;  /* gt_neighbour_mode */
 } gt_space;
@@ -105,8 +112,8 @@ int neighbours(const gt_space* sp, const gt_config* s, gt_config* out, int cap,
                int* n_out);
 
 /* C = A·B on the GPU with the kernel the configuration lowers to (§3.2, the
- * operator being tuned). A: M×K row-major, B: K×N row-major (dtype), C: M×N
- * row-major fp32, all device pointers. stream: hipStream_t (NULL = default).
+ * operator being tuned). A: M×K row-major (K×M with GT_A_KMAJOR in dtype),
+ * B: K×N row-major (dtype), C: M×N row-major fp32, all device pointers. stream: hipStream_t (NULL = default).
  * Asynchronous; C is overwritten. The configuration's products must equal
  * M, K, N and it must be legitimate in the space (M, N, K, cfg->d_*, dtype,
  * mfma_coord = cfg->mfma != 0). */

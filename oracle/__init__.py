@@ -121,6 +121,17 @@ def gemm(A_bytes: np.ndarray, B_bytes: np.ndarray, M: int, N: int, K: int, dtype
     return C
 
 
+def gemm_tn(W_bytes: np.ndarray, B_bytes: np.ndarray, M: int, N: int, K: int, dtype,
+            nthreads: int | None = None) -> np.ndarray:
+    """The perceptron product of §5, Y = WᵀX with W (K×M) and X (K×N) given as
+    raw row-major bytes: A = Wᵀ element by element (a byte-exact transpose),
+    then the plain product."""
+    esz = 4 if _dtype_code(dtype) == F32 else 2
+    W = np.ascontiguousarray(W_bytes, dtype=np.uint8).reshape(K, M, esz)
+    A_bytes = np.ascontiguousarray(W.transpose(1, 0, 2)).reshape(-1)
+    return gemm(A_bytes, B_bytes, M, N, K, dtype, nthreads)
+
+
 def gemm_entries(A_bytes, B_bytes, M, N, K, dtype, rows, cols) -> np.ndarray:
     dt = _dtype_code(dtype)
     rows = np.ascontiguousarray(rows, dtype=np.int64)

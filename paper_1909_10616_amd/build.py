@@ -46,6 +46,10 @@ def _units():
                     continue
                 units.append((f"gemm_{dn}_{i}_c{cpr}", "gemm_inst.hip",
                               [f"-DGT_DT={dt}", f"-DGT_I={i}", f"-DGT_CPR={cpr}"]))
+                if cpr and dt == 0:  # fp32 fast path for a K-major A
+                    units.append((f"gemm_{dn}_{i}_c{cpr}_akm", "gemm_inst.hip",
+                                  [f"-DGT_DT={dt}", f"-DGT_I={i}", f"-DGT_CPR={cpr}",
+                                   "-DGT_AKM=1"]))
     return units
 
 

@@ -22,15 +22,19 @@ __device__ __forceinline__ float load_in(const void* p, int64_t i, int dtype) {
   return __builtin_bit_cast(float, bits);
 }
 
-// One thread per output; k ascending, fp32 fused multiply-add.
+// One thread per output; k ascending, fp32 fused multiply-add. dtype 0/1
+// (fp32/bf16), plus 16 when A is K-major (element (m, k) at A[k·M + m]).
 __global__ void reference_kernel(const void* __restrict__ A, const void* __restrict__ B,
                                  float* __restrict__ C, int64_t M, int64_t N, int64_t K,
                                  int dtype) {
   const int64_t col = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   const int64_t row = static_cast<int64_t>(blockIdx.y) * blockDim.y + threadIdx.y;
   if (row >= M || col >= N) return;
+  const int dt = dtype & 15;
+  const int64_t sr = (dtype & 16) ? 1 : K, sk = (dtype & 16) ? M : 1;
   float s = 0.0f;
-  for (int64_t l = 0; l < K; ++l) s = fmaf(load_in(A, row * K + l, dtype), load_in(B, l * N + col, dtype), s);
+  for (int64_t l = 0; l < K; ++l)
+    s = fmaf(load_in(A, row * sr + l * sk, dt), load_in(B, l * N + col, dt), s);
   C[row * N + col] = s;
 }
 

@@ -43,6 +43,8 @@ struct KArgs {
   int32_t aVec, bVec;      // generic path: 1 or 16-byte vector tile loads
   int32_t dl;              // fast path: direct global->LDS loads into a ring
   int32_t ns;              // ring stages (direct-load path)
+  int32_t aKM;             // A given K-major (K×M row-major, element (m, k) at A[k·M + m])
+  int32_t lgBM;
 };
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
@@ -175,8 +177,13 @@ __device__ void gemm_generic(const KArgs& a, char* smem) {
 
   T* As0 = reinterpret_cast<T*>(smem);
   const int stage = (a.BM + a.BN) * a.BK;
-  const T* Ag = reinterpret_cast<const T*>(a.A) + static_cast<int64_t>(gm) * a.BM * a.K;
+  // A K-major: the tile is BK rows of BM contiguous m, kept as [k][m] in LDS
+  const bool akm = a.aKM != 0;
+  const T* Ag = reinterpret_cast<const T*>(a.A) +
+                (akm ? static_cast<int64_t>(gm) * a.BM : static_cast<int64_t>(gm) * a.BM * a.K);
   const T* Bg = reinterpret_cast<const T*>(a.B) + static_cast<int64_t>(gn) * a.BN;
+  // LDS element offsets of A (row r, k) = r·sr + k·sk
+  const int sr = akm ? 1 : a.BK, sk = akm ? a.BM : 1;
 
   // Rows of A / columns of B this lane feeds into each MFMA tile.
   int arow[TM], bcol[TN];
@@ -205,7 +212,10 @@ __device__ void gemm_generic(const KArgs& a, char* smem) {
     const int64_t kbase = (static_cast<int64_t>(l) * a.kSplit + z) * a.BK;
     T* as = As0 + buf * stage;
     T* bs = as + a.BM * a.BK;
-    copy_tile<T, Elem<DT>::VEC>(as, Ag + kbase, a.K, a.BM, a.BK, a.lgBK, a.aVec, tid, nthr);
+    if (akm)
+      copy_tile<T, Elem<DT>::VEC>(as, Ag + kbase * a.M, a.M, a.BK, a.BM, a.lgBM, a.aVec, tid, nthr);
+    else
+      copy_tile<T, Elem<DT>::VEC>(as, Ag + kbase, a.K, a.BM, a.BK, a.lgBK, a.aVec, tid, nthr);
     copy_tile<T, Elem<DT>::VEC>(bs, Bg + kbase * a.N, a.N, a.BK, a.BN, a.lgBN, a.bVec, tid, nthr);
   };
 
@@ -224,7 +234,7 @@ __device__ void gemm_generic(const KArgs& a, char* smem) {
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
               const int kl = kl0 + e;
-              v[e] = (aok[t] && kl < a.kBlk) ? as[arow[t] * a.BK + s * a.kBlk + kl] : uint16_t(0);
+              v[e] = (aok[t] && kl < a.kBlk) ? as[arow[t] * sr + (s * a.kBlk + kl) * sk] : uint16_t(0);
             }
             af[t] = __builtin_bit_cast(bf16x8, v);
           }
@@ -247,7 +257,7 @@ __device__ void gemm_generic(const KArgs& a, char* smem) {
           const bool kin = kl0 < a.kBlk;
 #pragma unroll
           for (int t = 0; t < TM; ++t)
-            af[t] = (aok[t] && kin) ? as[arow[t] * a.BK + s * a.kBlk + kl0] : 0.0f;
+            af[t] = (aok[t] && kin) ? as[arow[t] * sr + (s * a.kBlk + kl0) * sk] : 0.0f;
 #pragma unroll
           for (int t = 0; t < TN; ++t)
             bfv[t] = (bok[t] && kin) ? bs[(s * a.kBlk + kl0) * a.BN + bcol[t]] : 0.0f;
@@ -339,7 +349,9 @@ constexpr int ilog2c() {
 // CPR = 16-byte chunks per LDS row = BK / VEC, a compile-time constant so
 // that the chunk-step loop unrolls: the fragments of chunk-step cs+1 are read
 // from LDS while the MFMAs of chunk-step cs run.
-template <int DT, int I, int TM, int TN, int CPR>
+// AK: A given K-major; its tile is loaded like B's (VEC×VEC blocks,
+// transposed in registers) into the same [m][k-chunk] LDS layout.
+template <int DT, int I, int TM, int TN, int CPR, bool AK = false>
 __device__ void gemm_fast(const KArgs& a, char* smem) {
   using T = typename Elem<DT>::T;
   using acc_t = typename AccT<I>::type;
@@ -367,7 +379,8 @@ __device__ void gemm_fast(const KArgs& a, char* smem) {
   const int stage = achunks + (a.BN << LGCPR);  // chunks per stage
   u32x4* lds = reinterpret_cast<u32x4*>(smem);
 
-  const T* Ag = reinterpret_cast<const T*>(a.A) + static_cast<int64_t>(gm) * a.BM * a.K;
+  const T* Ag = reinterpret_cast<const T*>(a.A) +
+                (AK ? static_cast<int64_t>(gm) * a.BM : static_cast<int64_t>(gm) * a.BM * a.K);
   const T* Bg = reinterpret_cast<const T*>(a.B) + static_cast<int64_t>(gn) * a.BN;
 
   const int rounds = max((achunks + nthr * kPfA - 1) / (nthr * kPfA),
@@ -396,16 +409,45 @@ __device__ void gemm_fast(const KArgs& a, char* smem) {
     bq0[i] = ((nb << LGV) << LGCPR) + kb;
   }
 
+  // K-major A: blocks of VEC k-rows × VEC m (one 16-byte chunk per row),
+  // kPfA / VEC of them per thread in the staging registers
+  constexpr int kPfAB = kPfA / VEC;
+  const int lgnbm = a.lgBM - LGV;
+  const int ablocks = CPR << lgnbm;
+  const int nab = __builtin_amdgcn_readfirstlane(min(kPfAB, (ablocks + nthr - 1) / nthr));
+  int64_t aoffk[kPfAB > 0 ? kPfAB : 1];
+  int aq0[kPfAB > 0 ? kPfAB : 1];
+  if constexpr (AK) {
+#pragma unroll
+    for (int i = 0; i < kPfAB; ++i) {
+      const int b = min(tid + i * nthr, ablocks - 1);
+      const int nm = b & ((1 << lgnbm) - 1), kb = b >> lgnbm;
+      aoffk[i] = static_cast<int64_t>(kb << LGV) * a.M + (nm << LGV);
+      aq0[i] = ((nm << LGV) << LGCPR) + kb;
+    }
+  }
+
   u32x4 ra[kPfA];
   u32x4 rb[kPfB * VEC];
 
   auto gload = [&](int l) __attribute__((always_inline)) {
     const int64_t kbase = (static_cast<int64_t>(l) * a.kSplit + z) * a.BK;
-    const T* ag = Ag + kbase + aoff0;
     const T* bg = Bg + kbase * a.N;
+    if constexpr (AK) {
+      const T* ag = Ag + kbase * a.M;
 #pragma unroll
-    for (int i = 0; i < kPfA; ++i)
-      if (i < na) ra[i] = *reinterpret_cast<const u32x4*>(ag + i * astride);
+      for (int i = 0; i < kPfAB; ++i)
+        if (i < nab) {
+#pragma unroll
+          for (int j = 0; j < VEC; ++j)
+            ra[i * VEC + j] = *reinterpret_cast<const u32x4*>(ag + aoffk[i] + j * a.M);
+        }
+    } else {
+      const T* ag = Ag + kbase + aoff0;
+#pragma unroll
+      for (int i = 0; i < kPfA; ++i)
+        if (i < na) ra[i] = *reinterpret_cast<const u32x4*>(ag + i * astride);
+    }
 #pragma unroll
     for (int i = 0; i < kPfB; ++i)
       if (i < nbb) {
@@ -418,9 +460,20 @@ __device__ void gemm_fast(const KArgs& a, char* smem) {
   auto lstore = [&](int buf) __attribute__((always_inline)) {
     u32x4* as = lds + buf * stage;
     u32x4* bs = as + achunks;
+    if constexpr (AK) {
 #pragma unroll
-    for (int i = 0; i < kPfA; ++i)
-      if (i < na) as[swz(ta + i * nthr)] = ra[i];
+      for (int i = 0; i < kPfAB; ++i)
+        if (i < nab) {
+          u32x4 t[VEC];
+          transpose_block<DT>(&ra[i * VEC], t);
+#pragma unroll
+          for (int j = 0; j < VEC; ++j) as[swz(aq0[i] + (j << LGCPR))] = t[j];
+        }
+    } else {
+#pragma unroll
+      for (int i = 0; i < kPfA; ++i)
+        if (i < na) as[swz(ta + i * nthr)] = ra[i];
+    }
 #pragma unroll
     for (int i = 0; i < kPfB; ++i)
       if (i < nbb) {
@@ -436,9 +489,22 @@ __device__ void gemm_fast(const KArgs& a, char* smem) {
     const int64_t kbase = (static_cast<int64_t>(l) * a.kSplit + z) * a.BK;
     u32x4* as = lds + buf * stage;
     u32x4* bs = as + achunks;
-    for (int e = tid; e < achunks; e += nthr)
-      as[swz(e)] = *reinterpret_cast<const u32x4*>(
-          Ag + static_cast<int64_t>(e >> LGCPR) * a.K + kbase + ((e & (CPR - 1)) << LGV));
+    if constexpr (AK) {
+      for (int b = tid; b < ablocks; b += nthr) {
+        const int nm = b & ((1 << lgnbm) - 1), kb = b >> lgnbm;
+        const T* src = Ag + (kbase + (kb << LGV)) * a.M + (nm << LGV);
+        u32x4 r[VEC], t[VEC];
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) r[j] = *reinterpret_cast<const u32x4*>(src + j * a.M);
+        transpose_block<DT>(r, t);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) as[swz((((nm << LGV) + j) << LGCPR) + kb)] = t[j];
+      }
+    } else {
+      for (int e = tid; e < achunks; e += nthr)
+        as[swz(e)] = *reinterpret_cast<const u32x4*>(
+            Ag + static_cast<int64_t>(e >> LGCPR) * a.K + kbase + ((e & (CPR - 1)) << LGV));
+    }
     for (int b = tid; b < bblocks; b += nthr) {
       const int nb = b & ((1 << lgnbn) - 1), kb = b >> lgnbn;
       const T* src = Bg + (kbase + (kb << LGV)) * a.N + (nb << LGV);
@@ -966,6 +1032,13 @@ __global__ void __launch_bounds__((launch_threads<I, TM, TN, CPR>())) gemm_kerne
     gemm_generic<DT, I, TM, TN>(a, smem);
 }
 
+// Register-staged fast path for a K-major A.
+template <int DT, int I, int TM, int TN, int CPR>
+__global__ void __launch_bounds__((launch_threads<I, TM, TN, CPR>())) gemm_kernel_akm(KArgs a) {
+  extern __shared__ u32x4 gt_smem[];
+  gemm_fast<DT, I, TM, TN, CPR, true>(a, reinterpret_cast<char*>(gt_smem));
+}
+
 // bf16 fast path with direct global→LDS loads: a kernel of its own, so that
 // its register allocation does not inherit the register-staged path's.
 template <int I, int TM, int TN, int CPR>
@@ -989,16 +1062,24 @@ hipError_t launch_one(F fn, bool& attr_set, const KArgs& a, dim3 grid, dim3 bloc
   return hipGetLastError();
 }
 
-template <int DT, int I, int TM, int TN, int CPR>
+// AKM: the translation unit instantiates the K-major-A fast path (it then
+// serves only launches with a.aKM set; the generic path handles both layouts).
+template <int DT, int I, int TM, int TN, int CPR, bool AKM = false>
 hipError_t launch_gemm(const KArgs& a, dim3 grid, dim3 block, size_t lds, hipStream_t s) {
-  if constexpr (DT == 1 && CPR > 0) {
-    if (a.dl) {
-      static bool attr_dl = false;
-      return launch_one(gemm_kernel_dl<I, TM, TN, CPR>, attr_dl, a, grid, block, lds, s);
+  if constexpr (AKM) {
+    static_assert(CPR > 0, "the K-major-A kernel is a fast-path kernel");
+    static bool attr_akm = false;
+    return launch_one(gemm_kernel_akm<DT, I, TM, TN, CPR>, attr_akm, a, grid, block, lds, s);
+  } else {
+    if constexpr (DT == 1 && CPR > 0) {
+      if (a.dl) {
+        static bool attr_dl = false;
+        return launch_one(gemm_kernel_dl<I, TM, TN, CPR>, attr_dl, a, grid, block, lds, s);
+      }
     }
+    static bool attr = false;
+    return launch_one(gemm_kernel<DT, I, TM, TN, CPR>, attr, a, grid, block, lds, s);
   }
-  static bool attr = false;
-  return launch_one(gemm_kernel<DT, I, TM, TN, CPR>, attr, a, grid, block, lds, s);
 }
 
 // (TM, TN) pairs with TM·TN ≤ 16 (I = 32) and ≤ 64 (I = 16): the register
@@ -1014,8 +1095,8 @@ hipError_t launch_gemm(const KArgs& a, dim3 grid, dim3 block, size_t lds, hipStr
 // Chunks per LDS row with a fast-path instantiation (BK = CPR·VEC).
 constexpr int kFastCpr[] = {2, 4, 8, 16};
 
-// Kernel of (dtype, I, CPR, TM, TN), CPR = 0 for the generic path; nullptr
-// when not instantiated.
-LaunchFn find_gemm_kernel(int dtype, int I, int cpr, int TM, int TN);
+// Kernel of (dtype, I, CPR, TM, TN), CPR = 0 for the generic path, akm for
+// the K-major-A fast path (f32 only); nullptr when not instantiated.
+LaunchFn find_gemm_kernel(int dtype, int I, int cpr, int TM, int TN, bool akm);
 
 }  // namespace gt

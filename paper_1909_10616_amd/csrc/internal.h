@@ -20,7 +20,8 @@ struct Space {
   Dim dim[3];  // m, k, n
   uint64_t n_mfma = 1;
   uint64_t size = 1;
-  int dtype = GT_F32;
+  int dtype = GT_F32;   // gt_dtype without the layout flag
+  bool a_kmajor = false;  // GT_A_KMAJOR: A given as its K×M transpose
   int mfma_coord = 0;
   int mode = GT_ADJACENT;
   int64_t ext[3] = {1, 1, 1};

@@ -58,14 +58,18 @@ int lower(const gt_config& c, int64_t M, int64_t N, int64_t K, int dtype, const 
     return GT_EILLEGIT;
   }
   Levels& L = out->L;
-  levels_of(c, dtype, &L);
-  const int vec = dtype == GT_BF16 ? 8 : 4;
+  const int dt = s.dtype;          // without the layout flag
+  const bool akm = s.a_kmajor;     // A given K-major (K×M)
+  levels_of(c, dt, &L);
+  const int vec = dt == GT_BF16 ? 8 : 4;
   const int G = 64 / L.I;
   const int64_t cpr = L.BK / vec;  // 16-byte chunks per LDS row
   const bool cpr_ok = L.BK % vec == 0 && (cpr == 2 || cpr == 4 || cpr == 8 || cpr == 16);
+  // (a K-major A needs 16-byte m chunks, M % vec; its fast path is fp32 only)
   const bool fast = L.blkM % L.I == 0 && L.blkN % L.I == 0 && L.kBlk % L.IK == 0 &&
                     L.BK % (vec * G) == 0 && cpr_ok && L.BN % vec == 0 && K % vec == 0 &&
-                    N % vec == 0 && L.W <= 8 && aligned16(A) && aligned16(B);
+                    N % vec == 0 && L.W <= 8 && aligned16(A) && aligned16(B) &&
+                    (!akm || (dt == GT_F32 && L.BM % vec == 0 && M % vec == 0));
   const int64_t stage_bytes = (L.BM * L.BK + L.BK * L.BN) * L.elem;
   const bool dbuf = L.kLoop >= 2 && 2 * stage_bytes <= kLdsMax;
   // bf16 fast path with direct global->LDS loads into a ring of ns stages:
@@ -75,7 +79,7 @@ int lower(const gt_config& c, int64_t M, int64_t N, int64_t K, int dtype, const 
   const int64_t achunks = L.BM * L.BK / 8, bchunks = L.BK * L.BN / 8;
   const int64_t dl_inst = (achunks + bchunks) / 64;
   const int64_t ns = std::min<int64_t>(8, kLdsMax / std::max<int64_t>(stage_bytes, 1));
-  const bool dl = fast && dtype == GT_BF16 && achunks % (64 * L.W) == 0 &&
+  const bool dl = fast && dt == GT_BF16 && !akm && achunks % (64 * L.W) == 0 &&
                   bchunks % (64 * L.W) == 0 && dl_inst / L.W <= dl_inst_cap(L.acc) && ns >= 2 &&
                   L.BM * K < (int64_t{1} << 31) && L.BK * N < (int64_t{1} << 31);
 
@@ -109,7 +113,12 @@ int lower(const gt_config& c, int64_t M, int64_t N, int64_t K, int dtype, const 
   a.dbuf = dbuf ? 1 : 0;
   a.atomic = L.kSplit > 1 ? 1 : 0;
   a.remap = (L.gridM * L.gridN) % 8 == 0 ? 1 : 0;
-  a.aVec = (L.BK % vec == 0 && K % vec == 0 && aligned16(A)) ? vec : 1;
+  a.aVec = (akm ? (L.BM % vec == 0 && M % vec == 0) : (L.BK % vec == 0 && K % vec == 0)) &&
+                   aligned16(A)
+               ? vec
+               : 1;
+  a.aKM = akm ? 1 : 0;
+  a.lgBM = ilog2(L.BM);
   a.bVec = (L.BN % vec == 0 && N % vec == 0 && aligned16(B)) ? vec : 1;
   a.dl = dl ? 1 : 0;
   a.ns = dl ? static_cast<int32_t>(ns) : 0;
@@ -118,8 +127,8 @@ int lower(const gt_config& c, int64_t M, int64_t N, int64_t K, int dtype, const 
   out->block = dim3(static_cast<unsigned>(64 * L.W), 1, 1);
   out->lds = static_cast<size_t>(stage_bytes * (dl ? ns : (dbuf ? 2 : 1)));
   out->fast = fast;
-  out->fn = find_gemm_kernel(dtype, L.I, fast ? static_cast<int>(cpr) : 0,
-                             static_cast<int>(L.TM), static_cast<int>(L.TN));
+  out->fn = find_gemm_kernel(dt, L.I, fast ? static_cast<int>(cpr) : 0,
+                             static_cast<int>(L.TM), static_cast<int>(L.TN), fast && akm);
   if (!out->fn) {
     set_error("no kernel instantiation for this MFMA tile shape");
     return GT_ENOKERNEL;
@@ -271,7 +280,8 @@ int gt_measure(const gt_config* cfg, const void* A, const void* B, void* C, int6
 
 int gt_reference_gemm(const void* A, const void* B, void* C, int64_t M, int64_t N, int64_t K,
                       int dtype, void* stream) {
-  if (!A || !B || !C || M < 1 || N < 1 || K < 1 || (dtype != GT_F32 && dtype != GT_BF16)) {
+  const int base = dtype & ~GT_A_KMAJOR;
+  if (!A || !B || !C || M < 1 || N < 1 || K < 1 || (base != GT_F32 && base != GT_BF16)) {
     gt::set_error("gt_reference_gemm: bad argument");
     return GT_EINVAL;
   }

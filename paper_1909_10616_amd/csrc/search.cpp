@@ -173,7 +173,8 @@ struct Tuner {
     g.K = sp->K;
     g.dtype = sp->dtype;
     g.s = static_cast<hipStream_t>(o->stream);
-    g.tol = sp->dtype == GT_F32 ? 1e-5 * std::sqrt(static_cast<double>(sp->K)) : 2e-3;
+    g.tol = (sp->dtype & ~GT_A_KMAJOR) == GT_F32 ? 1e-5 * std::sqrt(static_cast<double>(sp->K))
+                                                   : 2e-3;
     g.c_ref = o->c_ref;
     if (o->check) {
       if (!g.c_ref) {

@@ -97,8 +97,9 @@ int make_space(const gt_space* sp, Space* s) {
   }
   const int64_t ext[3] = {sp->M, sp->K, sp->N};
   const int32_t d[3] = {sp->d_m, sp->d_k, sp->d_n};
-  if (sp->dtype != GT_F32 && sp->dtype != GT_BF16) {
-    set_error("space: dtype must be GT_F32 or GT_BF16");
+  const int base = sp->dtype & ~GT_A_KMAJOR;
+  if (base != GT_F32 && base != GT_BF16) {
+    set_error("space: dtype must be GT_F32 or GT_BF16 (optionally | GT_A_KMAJOR)");
     return GT_EINVAL;
   }
   if (sp->mfma_coord != 0 && sp->mfma_coord != 1) {
@@ -130,7 +131,8 @@ int make_space(const gt_space* sp, Space* s) {
   }
   s->n_mfma = sp->mfma_coord ? 2 : 1;
   s->size *= s->n_mfma;
-  s->dtype = sp->dtype;
+  s->dtype = base;
+  s->a_kmajor = (sp->dtype & GT_A_KMAJOR) != 0;
   s->mfma_coord = sp->mfma_coord;
   s->mode = sp->neighbour_mode;
   return GT_OK;

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(_PKG, "_lib", "libgemmtune.so")
 MAXD = 4
 
 F32, BF16 = 0, 1
+A_KMAJOR = 16  # dtype flag: A passed as its K×M transpose W, C = WᵀB
 ADJACENT, ANY_PAIR = 0, 1
 STATUS = {0: "ok", 1: "early-abort", 2: "launch-failure", 3: "mismatch"}
 STOP = {0: "budget", 1: "queue-empty", 2: "time-limit", 3: "draws-exhausted"}
@@ -156,13 +157,15 @@ def from_c(c: gt_config):
 
 
 class Space:
-    """Configuration space ξ (§3.3 Eq.1–4) with the C-ABI's queries."""
+    """Configuration space ξ (§3.3 Eq.1–4) with the C-ABI's queries.
+    a_kmajor: the problem's A is passed as W = Aᵀ (K×M), C = WᵀB (§5)."""
 
     def __init__(self, M, N, K, d=(4, 4, 4), dtype="f32", mfma_coord=False,
-                 mode=ADJACENT):
+                 mode=ADJACENT, a_kmajor=False):
         self.M, self.N, self.K = int(M), int(N), int(K)
         self.d = tuple(int(x) for x in d)
-        self.dtype = dtype_code(dtype)
+        self.dtype = dtype_code(dtype) | (A_KMAJOR if a_kmajor else 0)
+        self.a_kmajor = bool(self.dtype & A_KMAJOR)
         self.mfma_coord = bool(mfma_coord)
         self.mode = int(mode)
         s = gt_space()
@@ -238,7 +241,9 @@ def _stream(stream):
     return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
 
 
-def _operands(A, B, C):
+def _operands(A, B, C, a_kmajor=False):
+    """(M, N, K, dtype code) of C = A·B, or of C = AᵀB when a_kmajor (A is
+    then the K×M array W)."""
     import torch
     for t, name in ((A, "A"), (B, "B"), (C, "C")):
         if not t.is_cuda or not t.is_contiguous():
@@ -247,22 +252,23 @@ def _operands(A, B, C):
         raise ValueError("A and B must both be float32 or both bfloat16")
     if C.dtype != torch.float32:
         raise ValueError("C must be float32")
-    M, K = A.shape
+    K, M = A.shape if a_kmajor else A.shape[::-1]
     K2, N = B.shape
     if K2 != K or tuple(C.shape) != (M, N):
         raise ValueError(f"shape mismatch A{tuple(A.shape)} B{tuple(B.shape)} C{tuple(C.shape)}")
-    return M, N, K, dtype_code(A.dtype)
+    return M, N, K, dtype_code(A.dtype) | (A_KMAJOR if a_kmajor else 0)
 
 
-def gemm_run(cfg, A, B, C, stream=None):
-    M, N, K, dt = _operands(A, B, C)
+def gemm_run(cfg, A, B, C, stream=None, a_kmajor=False):
+    M, N, K, dt = _operands(A, B, C, a_kmajor)
     _check(lib().gemm_run(ctypes.byref(to_c(cfg)), A.data_ptr(), B.data_ptr(), C.data_ptr(), M, N,
                           K, dt, _stream(stream)), "gemm_run")
     return C
 
 
-def gt_measure(cfg, A, B, C, warmup=1, runs=10, abort_ms=0.0, stream=None) -> dict:
-    M, N, K, dt = _operands(A, B, C)
+def gt_measure(cfg, A, B, C, warmup=1, runs=10, abort_ms=0.0, stream=None,
+               a_kmajor=False) -> dict:
+    M, N, K, dt = _operands(A, B, C, a_kmajor)
     mean, first, ab = ctypes.c_double(), ctypes.c_double(), ctypes.c_int()
     _check(lib().gt_measure(ctypes.byref(to_c(cfg)), A.data_ptr(), B.data_ptr(), C.data_ptr(), M,
                             N, K, dt, _stream(stream), warmup, runs, abort_ms, ctypes.byref(mean),
@@ -270,8 +276,8 @@ def gt_measure(cfg, A, B, C, warmup=1, runs=10, abort_ms=0.0, stream=None) -> di
     return {"mean_ms": mean.value, "first_ms": first.value, "aborted": bool(ab.value)}
 
 
-def gt_reference_gemm(A, B, C, stream=None):
-    M, N, K, dt = _operands(A, B, C)
+def gt_reference_gemm(A, B, C, stream=None, a_kmajor=False):
+    M, N, K, dt = _operands(A, B, C, a_kmajor)
     _check(lib().gt_reference_gemm(A.data_ptr(), B.data_ptr(), C.data_ptr(), M, N, K, dt,
                                    _stream(stream)), "gt_reference_gemm")
     return C
@@ -306,7 +312,7 @@ def _tune(entry, space: Space, budget: int, s0, rho, seed, runs, warmup, check, 
             return float(cost_fn(from_c(cptr.contents), int(rank)))
         keep = cb = gt_cost_fn(_cb)
     else:
-        M, N, K, dt = _operands(A, B, C)
+        M, N, K, dt = _operands(A, B, C, space.a_kmajor)
         if (M, N, K, dt) != (space.M, space.N, space.K, space.dtype):
             raise ValueError("operands do not match the space")
         o.A, o.B, o.C = A.data_ptr(), B.data_ptr(), C.data_ptr()

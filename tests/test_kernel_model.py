@@ -1,7 +1,8 @@
 """A CPU model of the fast-path and direct-load GEMM kernels' addressing and
 of the direct-load ring schedule, run over seeded samples of the configurations
-of the 1024³ and 4096³ bf16 spaces that meet the fast path's shape conditions
-(plus the known fastest 4096³ configurations). The same model run over all
+of the 1024³ and 4096³ bf16 spaces and of the 2048³ fp32 space (A row-major
+and K-major) that meet the fast path's shape conditions (plus the known
+fastest 4096³ configurations). The same model run over all
 98,086 such configurations of the 4096³ space finds no violation.
 
 For each configuration the model takes the launch the library chose
@@ -122,8 +123,8 @@ def check_c_and_frags(L, CPR, achunks, lane, bt_rows=None):
         assert cols.max() < L["BN"]
 
 
-def check_fast(L, info, M, N, K):
-    VEC, LGV = 8, 3
+def check_fast(L, info, M, N, K, vec=8, akm=False):
+    VEC, LGV = vec, lg(vec)
     CPR = L["BK"] // VEC
     LGCPR = lg(CPR)
     nthr = 64 * L["W"]
@@ -138,7 +139,24 @@ def check_fast(L, info, M, N, K):
     for gm, gn, z, l in tiles(L):
         kbase = (l * L["kSplit"] + z) * L["BK"]
         a0, b0 = gm * BM * K + kbase, gn * BN + kbase * N
-        if prefetch:
+        if akm:
+            # A K-major: VEC×VEC blocks of W (K×M), like B's
+            lgnbm = lg(BM) - LGV
+            ablocks = CPR << lgnbm
+            if prefetch:
+                nab = min(8 // VEC, -(-ablocks // nthr))
+                ab = np.concatenate([np.minimum(tid + i * nthr, ablocks - 1) for i in range(nab)])
+            else:
+                ab = np.arange(ablocks)
+            nm, kb = ab & ((1 << lgnbm) - 1), ab >> lgnbm
+            for j in range(VEC):
+                addr = gm * BM + (kbase + (kb << LGV) + j) * M + (nm << LGV)
+                assert addr.min() >= 0 and addr.max() + VEC <= K * M
+                assert swz((((nm << LGV) + j) << LGCPR) + kb).max() < achunks
+            # every A chunk of the stage is written
+            dst = np.concatenate([swz((((nm << LGV) + j) << LGCPR) + kb) for j in range(VEC)])
+            assert len(np.unique(dst)) == achunks
+        elif prefetch:
             ta = np.minimum(tid, achunks - 1)
             na = min(8, -(-achunks // nthr))
             for i in range(na):
@@ -146,12 +164,11 @@ def check_fast(L, info, M, N, K):
                 addr = a0 + (ta >> LGCPR) * K + ((ta & (CPR - 1)) << LGV) + i * (nthr >> LGCPR) * K
                 assert addr.min() >= 0 and addr.max() + VEC <= M * K
                 assert swz(e).max() < achunks
-            b = np.minimum(tid, bblocks - 1)
         else:
             e = np.arange(achunks)
             addr = a0 + (e >> LGCPR) * K + ((e & (CPR - 1)) << LGV)
             assert addr.max() + VEC <= M * K and swz(e).max() < achunks
-            b = np.arange(bblocks)
+        b = np.minimum(tid, bblocks - 1) if prefetch else np.arange(bblocks)
         nb, kb = b & ((1 << lgnbn) - 1), b >> lgnbn
         for j in range(VEC):
             addr = b0 + ((kb << LGV) + j) * N + (nb << LGV)
@@ -292,40 +309,53 @@ def _tuples(D, d):
             if sum(es) == E]
 
 
-def fast_candidates(D):
-    """Configurations of the D³ bf16 space (d = 4, MFMA coordinate) that
-    meet the fast path's shape conditions."""
+def fast_candidates(D, dtype="bf16"):
+    """Configurations of the D³ space (d = 4; bf16 with the MFMA coordinate,
+    fp32 without) that meet the fast path's shape conditions."""
     T = _tuples(D, 4)
     out = []
-    for mf in (16, 32):
-        G, IK = 64 // mf, (16 if mf == 32 else 32)
-        Ms = [t for t in T if t[3] % mf == 0]
-        Ks = [k for k in T if k[3] % IK == 0 and (k[2] * k[3]) % (8 * G) == 0
-              and (k[2] * k[3]) // 8 in (2, 4, 8, 16)]
-        for m, n in itertools.product(Ms, Ms):
-            W = m[1] * n[1]
-            acc = m[2] * (m[3] // mf) * n[2] * (n[3] // mf) * mf * mf // 64
-            if W > 8 or acc > 256 or acc + 96 > 512 // ((W + 3) // 4):
-                continue
-            BM, BN = m[1] * m[2] * m[3], n[1] * n[2] * n[3]
-            out += [(m, k, n, mf) for k in Ks if (BM + BN) * k[2] * k[3] * 2 <= LDS_MAX]
+    vec, esz = (8, 2) if dtype == "bf16" else (4, 4)
+    for mf in ((16, 32) if dtype == "bf16" else (0,)):
+        for I in ((mf,) if mf else (16, 32)):
+            out += _fast_for(T, I, mf, vec, esz)
     return out
 
 
-def _run(gt, cfgs, D):
+def _fast_for(T, I, mf, vec, esz):
+    G = 64 // I
+    IK = (16 if I == 32 else 32) if vec == 8 else (2 if I == 32 else 4)
+    Ms = [t for t in T if t[3] % I == 0]
+    Ks = [k for k in T if k[3] % IK == 0 and (k[2] * k[3]) % (vec * G) == 0
+          and (k[2] * k[3]) // vec in (2, 4, 8, 16)]
+    out = []
+    for m, n in itertools.product(Ms, Ms):
+        if not mf and (I == 32) != (m[3] % 32 == 0 and n[3] % 32 == 0):
+            continue  # fp32: I is 32 exactly when both blocks are multiples of 32
+        W = m[1] * n[1]
+        acc = m[2] * (m[3] // I) * n[2] * (n[3] // I) * I * I // 64
+        if W > 8 or acc > 256 or acc + 96 > 512 // ((W + 3) // 4):
+            continue
+        BM, BN = m[1] * m[2] * m[3], n[1] * n[2] * n[3]
+        out += [(m, k, n, mf) for k in Ks if (BM + BN) * k[2] * k[3] * esz <= LDS_MAX]
+    return out
+
+
+def _run(gt, cfgs, D, dtype="bf16", akm=False):
     n = {"dl": 0, "fast": 0}
+    code = gt.dtype_code(dtype) | (gt.A_KMAJOR if akm else 0)
     for c in cfgs:
         try:
-            info = gt.lower(c, D, D, D, "bf16")
+            info = gt.lower(c, D, D, D, code)
         except gt.GemmTuneError:
             continue  # (TM, TN) without an instantiation
         L = levels(c)
         assert (info["BM"], info["BN"], info["BK"], info["waves"]) == (L["BM"], L["BN"], L["BK"], L["W"])
         if info["dl"]:
+            assert not akm
             check_dl(L, info, D, D, D)
             n["dl"] += 1
         elif info["fast"]:
-            check_fast(L, info, D, D, D)
+            check_fast(L, info, D, D, D, vec=8 if dtype == "bf16" else 4, akm=akm)
             n["fast"] += 1
     return n
 
@@ -344,6 +374,14 @@ def test_model_sample_4096(gt):
     sample = known + random.Random(5).sample(cands, 3000)
     n = _run(gt, sample, 4096)
     assert n["dl"] > 100 and n["fast"] > 100, n
+
+
+@pytest.mark.parametrize("akm", [False, True])
+def test_model_sample_f32(gt, akm):
+    """fp32 register-staged path, A row-major and K-major (2048³)."""
+    cands = fast_candidates(2048, "f32")
+    n = _run(gt, random.Random(6).sample(cands, min(2000, len(cands))), 2048, "f32", akm)
+    assert n["fast"] > 500 and n["dl"] == 0, n
 
 
 @pytest.mark.parametrize("ns", range(2, 9))

@@ -80,6 +80,30 @@ def make_inputs(M: int, N: int, K: int, dtype: str, seed: int, dist: str):
     return A.contiguous(), B.contiguous()
 
 
+# The paper's own protocol (§5): perceptron layers Y = WᵀX of sizes
+# (m, k, n) = 512³, 1024³, 2048³ in fp32, d = (4, 2, 4), neighbours between
+# any two levels (Eq.6), s0 = [[m,1,1,1],[k,1],[n,1,1,1]], ρ = 5, and a budget
+# of 0.1 % of the space: ⌈0.001·|ξ|⌉ of 484,000, 899,756 and 1,589,952.
+PAPER_PROTOCOL = [
+    Workload("perceptron512_f32", 512, 512, 512, F32, 0, "uniform", (4, 2, 4), False, 484),
+    Workload("perceptron1024_f32", 1024, 1024, 1024, F32, 0, "uniform", (4, 2, 4), False, 900),
+    Workload("perceptron2048_f32", 2048, 2048, 2048, F32, 0, "uniform", (4, 2, 4), False, 1590),
+]
+
+
+def make_perceptron_inputs(M: int, N: int, K: int, dtype: str, seed: int, dist: str):
+    """Host tensors of the perceptron layer Y = WᵀX of §5: W (K×M) drawn
+    first, then X (K×N), row-major, in the input dtype."""
+    gen = torch.Generator().manual_seed(seed)
+    W = _draw(gen, (K, M), dist, K)
+    X = _draw(gen, (K, N), dist, K)
+    if dtype == BF16:
+        W, X = W.to(torch.bfloat16), X.to(torch.bfloat16)
+    elif dtype != F32:
+        raise ValueError(f"unknown dtype {dtype!r}")
+    return W.contiguous(), X.contiguous()
+
+
 def workload_inputs(w: Workload):
     return make_inputs(w.M, w.N, w.K, w.dtype, w.seed, w.dist)
 
