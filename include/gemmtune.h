@@ -193,6 +193,7 @@ typedef struct gt_tune_opts {
   void* stream;
   gt_log_entry* log;     /* optional, caller-owned, log_cap entries */
   int64_t log_cap;
+  double progress_s;     /* > 0: a progress line on stderr at most this often */
 } gt_tune_opts;
 
 typedef struct gt_tune_result {

@@ -15,6 +15,7 @@
 
 #include <chrono>
 #include <cmath>
+#include <cstdio>
 #include <cstring>
 #include <queue>
 #include <string>
@@ -135,6 +136,8 @@ struct Tuner {
   GpuCtx g{};
   void* owned_ref = nullptr;
   double cost_min = INFINITY;
+  double last_progress = 0.0;
+  const char* who = "";
   std::chrono::steady_clock::time_point t0 = std::chrono::steady_clock::now();
 
   ~Tuner() {
@@ -153,6 +156,7 @@ struct Tuner {
       return GT_EINVAL;
     }
     o = opts;
+    this->who = who;
     cost = cb;
     ctx = cb_ctx;
     out = res;
@@ -214,6 +218,16 @@ struct Tuner {
     if (o->log && out->timed < o->log_cap) o->log[out->timed] = rec;
     ++out->timed;
     if (std::isinf(v)) ++out->failed;
+    if (o->progress_s > 0.0) {
+      const double t = elapsed();
+      if (t - last_progress >= o->progress_s) {
+        last_progress = t;
+        std::fprintf(stderr, "[gemmtune] %s: %lld of %lld timed, best %.4f ms, %.1f s\n", who,
+                     static_cast<long long>(out->timed), static_cast<long long>(o->budget),
+                     std::min(cost_min, v), t);
+        std::fflush(stderr);
+      }
+    }
     return v;
   }
 

@@ -67,7 +67,8 @@ class gt_tune_opts(ctypes.Structure):
                 ("abort_factor", ctypes.c_double),
                 ("A", ctypes.c_void_p), ("B", ctypes.c_void_p), ("C", ctypes.c_void_p),
                 ("c_ref", ctypes.c_void_p), ("stream", ctypes.c_void_p),
-                ("log", ctypes.POINTER(gt_log_entry)), ("log_cap", ctypes.c_int64)]
+                ("log", ctypes.POINTER(gt_log_entry)), ("log_cap", ctypes.c_int64),
+                ("progress_s", ctypes.c_double)]
 
 
 class gt_tune_result(ctypes.Structure):
@@ -292,7 +293,7 @@ def gt_compare(C, R, stream=None) -> float:
 
 
 def _tune(entry, space: Space, budget: int, s0, rho, seed, runs, warmup, check, t_max_s,
-          max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream) -> dict:
+          max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream, progress_s=0.0) -> dict:
     L = lib()
     o = gt_tune_opts()
     _check(L.gt_tune_opts_init(ctypes.byref(o)), "gt_tune_opts_init")
@@ -302,6 +303,7 @@ def _tune(entry, space: Space, budget: int, s0, rho, seed, runs, warmup, check, 
     o.rho, o.runs, o.warmup, o.check = rho, runs, warmup, int(check)
     o.budget, o.t_max_s, o.seed = budget, t_max_s, seed
     o.max_run_ms, o.abort_factor = max_run_ms, abort_factor
+    o.progress_s = progress_s
     log = (gt_log_entry * budget)()
     o.log = ctypes.cast(log, ctypes.POINTER(gt_log_entry))
     o.log_cap = budget
@@ -337,22 +339,23 @@ def _tune(entry, space: Space, budget: int, s0, rho, seed, runs, warmup, check, 
 def tune_gbfs(space: Space, budget: int, s0=None, rho: int = 5, seed: int = 0, runs: int = 10,
               warmup: int = 1, check: bool = True, t_max_s: float = 0.0,
               max_run_ms: float = 250.0, abort_factor: float = 50.0, A=None, B=None, C=None,
-              c_ref=None, cost_fn=None, stream=None) -> dict:
+              c_ref=None, cost_fn=None, stream=None, progress_s: float = 0.0) -> dict:
     """Run G-BFS (Alg.1). With ``cost_fn(cfg, rank) -> float`` the costs are
     synthetic (no GPU); otherwise A, B, C are GPU tensors and every candidate
-    is timed with ``gemm_run`` on the stream."""
+    is timed with ``gemm_run`` on the stream (A is W, K×M, when the space has
+    a_kmajor). progress_s > 0: a progress line on stderr at most that often."""
     return _tune("tune_gbfs", space, budget, s0, rho, seed, runs, warmup, check, t_max_s,
-                 max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream)
+                 max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream, progress_s)
 
 
 def tune_random(space: Space, budget: int, seed: int = 0, runs: int = 10, warmup: int = 1,
                 check: bool = True, t_max_s: float = 0.0, max_run_ms: float = 250.0,
                 abort_factor: float = 50.0, A=None, B=None, C=None, c_ref=None, cost_fn=None,
-                stream=None) -> dict:
+                stream=None, progress_s: float = 0.0) -> dict:
     """Equal-budget random search (§5 baseline); same timing and result as
     tune_gbfs, ``popped`` counts the draws."""
     return _tune("tune_random", space, budget, None, 1, seed, runs, warmup, check, t_max_s,
-                 max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream)
+                 max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream, progress_s)
 
 
 def tflops(M, N, K, ms) -> float:
