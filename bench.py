@@ -6,10 +6,11 @@ configurations — enumeration/rank, legitimacy, neighbours, ρ-sampling,
 lowering, every candidate GEMM run and timed on the GPU and checked against
 the reference — followed by the report: s* and the next TOPK − 1 configurations of
 the search log by cost, each re-timed over REPEAT back-to-back launches
-between HIP events on the bench stream; the fastest is reported.
+between HIP events on the bench stream; the fastest is the reported
+configuration, and it is re-timed once more (REPEAT launches) for the value.
 
-value   = TFLOP/s of the reported configuration (2·M·N·K per run) from its
-          re-timing;
+value   = TFLOP/s of the reported configuration (2·M·N·K per run) from that
+          last re-timing;
 ms_per_step = wall time of one step (search + report).
 
 Prints ONE JSON line (rank 0). Only one GPU: --gpus above 1 exits.
@@ -256,15 +257,18 @@ def main():
                                A=Ad, B=Bd, C=C, c_ref=Cref, stream=stream)
             # report: the TOPK configurations of the log with the lowest
             # (10-run) costs are re-timed over REPEAT launches each, s* first;
-            # the fastest re-timing is the reported configuration
+            # the fastest is the reported configuration
             ok = sorted((e["cost_ms"], e["rank"]) for e in res["log"] if e["status"] == "ok")
             ranks = [res["best_rank"]] + [r for _, r in ok if r != res["best_rank"]][:TOPK - 1]
             top = []
             for r in ranks:
                 cfg = sp.unrank(r)
                 top.append((retime(cfg), r, cfg))
-            best_ms, best_rank, best = min(top)
-            gt.gemm_run(best, Ad, Bd, C, stream=stream)   # C of the reported configuration
+            _, best_rank, best = min(top)
+            # the reported time is a fresh re-timing of the chosen configuration
+            # (not the minimum the choice was made on), and the trace's last
+            # dispatches are the reported configuration's
+            best_ms = retime(best)
         res["search_best"], res["search_best_rank"] = res["best"], res["best_rank"]
         res["best"], res["best_rank"], res["best_ms"] = best, best_rank, best_ms
         res["top"] = [(fmt_cfg(c), round(ms * 1e3, 2)) for ms, _, c in top]
