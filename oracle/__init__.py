@@ -57,6 +57,18 @@ class _GbfsResult(ctypes.Structure):
                 ("timed", ctypes.c_int64), ("popped", ctypes.c_int64)]
 
 
+class _Na2cParams(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int32), ("B", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("mem", ctypes.c_int32), ("max_walks", ctypes.c_int32),
+                ("eps", ctypes.c_double), ("gamma", ctypes.c_double), ("lr", ctypes.c_double),
+                ("r_clip", ctypes.c_double)]
+
+
+# N-A2C settings: T = 3 steps per walk (§5), the rest are readings
+NA2C_DEFAULTS = dict(T=3, B=8, H=32, mem=256, max_walks=64, eps=0.8, gamma=0.9, lr=0.01,
+                     r_clip=5.0)
+
+
 _COST_FN = ctypes.CFUNCTYPE(ctypes.c_double, ctypes.POINTER(_Config), ctypes.c_uint64,
                             ctypes.c_void_p)
 
@@ -89,6 +101,11 @@ def lib():
                               ctypes.POINTER(_GbfsResult), p, p, i64]
         L.or_random_search.argtypes = [SP, i64, u64, _COST_FN, p, ctypes.POINTER(_GbfsResult),
                                        p, p, i64]
+        NP = ctypes.POINTER(_Na2cParams)
+        L.or_na2c.argtypes = [SP, CF, NP, i64, u64, _COST_FN, p, ctypes.POINTER(_GbfsResult),
+                              p, p, i64]
+        L.or_na2c_probe.argtypes = [SP, NP, u64, CF, ctypes.c_int, p, p, p, p, p, p,
+                                    ctypes.POINTER(i64), ctypes.POINTER(i64)]
         _lib = L
     return _lib
 
@@ -306,3 +323,56 @@ def random_search(space: Space, budget: int, seed: int, cost_fn):
     return {"best": space._from_c(res.best), "best_cost": float(res.best_cost),
             "timed": n, "popped": int(res.popped),
             "log_ranks": [int(v) for v in log_r[:n]], "log_costs": [float(v) for v in log_c[:n]]}
+
+
+def _na2c_params(params=None) -> _Na2cParams:
+    v = dict(NA2C_DEFAULTS)
+    v.update(params or {})
+    return _Na2cParams(**v)
+
+
+def na2c(space: Space, s0, budget: int, seed: int, cost_fn, params=None):
+    """N-A2C (§4.3, Alg.2) with the oracle's readings; ``params`` overrides
+    NA2C_DEFAULTS. Same result dict as gbfs(); ``popped`` counts episodes."""
+    log_r = np.zeros(budget, dtype=np.uint64)
+    log_c = np.zeros(budget, dtype=np.float64)
+
+    def _cb(cptr, rank, _ctx):
+        return float(cost_fn(space._from_c(cptr.contents), int(rank)))
+
+    cb = _COST_FN(_cb)
+    res = _GbfsResult()
+    prm = _na2c_params(params)
+    rc = lib().or_na2c(ctypes.byref(space._s), ctypes.byref(space._to_c(s0)), ctypes.byref(prm),
+                       int(budget), int(seed), cb, None, ctypes.byref(res), _ptr(log_r),
+                       _ptr(log_c), budget)
+    if rc:
+        raise ValueError("or_na2c: bad argument")
+    n = int(res.timed)
+    return {"best": space._from_c(res.best), "best_cost": float(res.best_cost),
+            "timed": n, "popped": int(res.popped),
+            "log_ranks": [int(v) for v in log_r[:n]], "log_costs": [float(v) for v in log_c[:n]]}
+
+
+def na2c_probe(space: Space, cfg, a: int, seed: int = 0, params=None, actor=None, critic=None):
+    """π(·|s), V(s), ∇θ log π(a|s) and ∇θ V(s) of the N-A2C networks, at the
+    initial weights of ``seed`` or at the given flattened parameters."""
+    prm = _na2c_params(params)
+    na, nc = ctypes.c_int64(), ctypes.c_int64()
+    assert lib().or_na2c_probe(ctypes.byref(space._s), ctypes.byref(prm), int(seed), None, 0,
+                               None, None, None, None, None, None, ctypes.byref(na),
+                               ctypes.byref(nc)) == 0
+    A = sum(d * (d - 1) if space.mode == ANY_PAIR else 2 * (d - 1) for d in space.d)
+    A += 1 if space.mfma_coord else 0
+    pi = np.zeros(64)
+    v = np.zeros(1)
+    ga, gc = np.zeros(na.value), np.zeros(nc.value)
+    ap = None if actor is None else np.ascontiguousarray(actor, dtype=np.float64)
+    cp = None if critic is None else np.ascontiguousarray(critic, dtype=np.float64)
+    rc = lib().or_na2c_probe(ctypes.byref(space._s), ctypes.byref(prm), int(seed),
+                             ctypes.byref(space._to_c(cfg)), int(a),
+                             None if ap is None else _ptr(ap), None if cp is None else _ptr(cp),
+                             _ptr(pi), _ptr(v), _ptr(ga), _ptr(gc), None, None)
+    assert rc == 0
+    return {"pi": pi[:A], "v": float(v[0]), "g_actor": ga, "g_critic": gc,
+            "n_actor": na.value, "n_critic": nc.value}

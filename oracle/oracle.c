@@ -577,3 +577,459 @@ int or_random_search(const or_space* sp, int64_t budget, uint64_t seed, or_cost_
   free_tables(&tb);
   return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* N-A2C (§4.3, Alg.2).                                                      */
+/* ------------------------------------------------------------------------ */
+
+typedef struct { /* one action of the fixed list: f[x][i] *= 2, f[x][j] /= 2, or the toggle */
+  int x, i, j, toggle;
+} na_action;
+
+typedef struct {
+  int F, A, H;
+  na_action act[3 * OR_MAXD * OR_MAXD + 1];
+  int E[3];
+  int64_t q[3];
+  /* actor */
+  double *W1, *b1, *W2, *b2;
+  /* critic */
+  double *U1, *c1, *u2, c2;
+} na_net;
+
+static void na_actions(const or_space* sp, na_net* n) {
+  n->A = 0;
+  for (int x = 0; x < 3; ++x)
+    for (int i = 0; i < sp->d[x]; ++i)
+      for (int j = 0; j < sp->d[x]; ++j) {
+        if (i == j) continue;
+        if (sp->mode == OR_ADJACENT && abs(i - j) != 1) continue;
+        na_action a = {x, i, j, 0};
+        n->act[n->A++] = a;
+      }
+  if (sp->mfma_coord) {
+    na_action a = {0, 0, 0, 1};
+    n->act[n->A++] = a;
+  }
+}
+
+static int na_log2(int64_t v) {
+  int e = 0;
+  while (v > 1) {
+    v >>= 1;
+    ++e;
+  }
+  return e;
+}
+
+/* φ(s): exponent share of every level (level 0 without the odd cofactor),
+ * then the MFMA bit. */
+static void na_features(const or_space* sp, const na_net* n, const or_config* s, double* phi) {
+  int k = 0;
+  for (int x = 0; x < 3; ++x)
+    for (int i = 0; i < sp->d[x]; ++i) {
+      const int64_t v = i == 0 ? s->f[x][0] / n->q[x] : s->f[x][i];
+      phi[k++] = n->E[x] ? (double)na_log2(v) / (double)n->E[x] : 0.0;
+    }
+  if (sp->mfma_coord) phi[k++] = s->mfma == 32 ? 1.0 : 0.0;
+}
+
+static int na_available(const na_net* n, const or_config* s, int a) {
+  const na_action* ac = &n->act[a];
+  if (ac->toggle) return 1;
+  return s->f[ac->x][ac->j] % 2 == 0;
+}
+
+static or_config na_step(const na_net* n, const or_config* s, int a) {
+  or_config t = *s;
+  const na_action* ac = &n->act[a];
+  if (ac->toggle) {
+    t.mfma = s->mfma == 16 ? 32 : 16;
+  } else {
+    t.f[ac->x][ac->i] = s->f[ac->x][ac->i] * 2;
+    t.f[ac->x][ac->j] = s->f[ac->x][ac->j] / 2;
+  }
+  return t;
+}
+
+/* the action that undoes a (from step(s, a) back to s) */
+static int na_inverse(const na_net* n, int a) {
+  const na_action* ac = &n->act[a];
+  if (ac->toggle) return a;
+  for (int b = 0; b < n->A; ++b)
+    if (!n->act[b].toggle && n->act[b].x == ac->x && n->act[b].i == ac->j && n->act[b].j == ac->i)
+      return b;
+  return -1;
+}
+
+static double na_uniform(uint64_t* st) {
+  return (double)(or_splitmix64_next(st) >> 11) * (1.0 / 9007199254740992.0);
+}
+
+static int na_alloc(const or_space* sp, const or_na2c_params* prm, uint64_t seed, na_net* n) {
+  memset(n, 0, sizeof(*n));
+  na_actions(sp, n);
+  n->F = sp->d[0] + sp->d[1] + sp->d[2] + (sp->mfma_coord ? 1 : 0);
+  n->H = prm->H;
+  const int64_t ext[3] = {sp->M, sp->K, sp->N};
+  for (int x = 0; x < 3; ++x) {
+    n->q[x] = odd_part(ext[x]);
+    n->E[x] = na_log2(ext[x] / n->q[x]);
+  }
+  const int F = n->F, A = n->A, H = n->H;
+  n->W1 = (double*)calloc((size_t)(H * F), sizeof(double));
+  n->b1 = (double*)calloc((size_t)H, sizeof(double));
+  n->W2 = (double*)calloc((size_t)(A * H), sizeof(double));
+  n->b2 = (double*)calloc((size_t)A, sizeof(double));
+  n->U1 = (double*)calloc((size_t)(H * F), sizeof(double));
+  n->c1 = (double*)calloc((size_t)H, sizeof(double));
+  n->u2 = (double*)calloc((size_t)H, sizeof(double));
+  if (!n->W1 || !n->b1 || !n->W2 || !n->b2 || !n->U1 || !n->c1 || !n->u2) return -1;
+  /* weights U(−1/√fan_in, 1/√fan_in) in the order W1, W2, U1, u2; biases 0 */
+  uint64_t ws = seed ^ 0xA2C0A2C0A2C0A2C0ULL;
+  const double bF = 1.0 / sqrt((double)F), bH = 1.0 / sqrt((double)H);
+  for (int k = 0; k < H * F; ++k) n->W1[k] = (2.0 * na_uniform(&ws) - 1.0) * bF;
+  for (int k = 0; k < A * H; ++k) n->W2[k] = (2.0 * na_uniform(&ws) - 1.0) * bH;
+  for (int k = 0; k < H * F; ++k) n->U1[k] = (2.0 * na_uniform(&ws) - 1.0) * bF;
+  for (int k = 0; k < H; ++k) n->u2[k] = (2.0 * na_uniform(&ws) - 1.0) * bH;
+  n->c2 = 0.0;
+  return 0;
+}
+
+static void na_free(na_net* n) {
+  free(n->W1);
+  free(n->b1);
+  free(n->W2);
+  free(n->b2);
+  free(n->U1);
+  free(n->c1);
+  free(n->u2);
+}
+
+/* actor forward: hidden h[H], π over the available actions (0 elsewhere) */
+static void na_actor(const na_net* n, const double* phi, const int* avail, double* h,
+                     double* pi) {
+  for (int k = 0; k < n->H; ++k) {
+    double z = n->b1[k];
+    for (int f = 0; f < n->F; ++f) z += n->W1[k * n->F + f] * phi[f];
+    h[k] = tanh(z);
+  }
+  double zmax = -INFINITY;
+  for (int a = 0; a < n->A; ++a) {
+    if (!avail[a]) {
+      pi[a] = 0.0;
+      continue;
+    }
+    double z = n->b2[a];
+    for (int k = 0; k < n->H; ++k) z += n->W2[a * n->H + k] * h[k];
+    pi[a] = z;
+    if (z > zmax) zmax = z;
+  }
+  double sum = 0.0;
+  for (int a = 0; a < n->A; ++a)
+    if (avail[a]) {
+      pi[a] = exp(pi[a] - zmax);
+      sum += pi[a];
+    }
+  for (int a = 0; a < n->A; ++a)
+    if (avail[a]) pi[a] /= sum;
+}
+
+static double na_critic(const na_net* n, const double* phi, double* g) {
+  double v = n->c2;
+  for (int k = 0; k < n->H; ++k) {
+    double z = n->c1[k];
+    for (int f = 0; f < n->F; ++f) z += n->U1[k * n->F + f] * phi[f];
+    g[k] = tanh(z);
+    v += n->u2[k] * g[k];
+  }
+  return v;
+}
+
+typedef struct {
+  double phi[3 * OR_MAXD + 1], phi2[3 * OR_MAXD + 1];
+  int avail[3 * OR_MAXD * OR_MAXD + 1];
+  int a;
+  double r;
+} na_trans;
+
+/* one transition: δ from the current critic, then the critic's and the
+ * actor's updates (both with gradients at the pre-update weights) */
+static void na_train_one(na_net* n, const na_trans* t, double gamma, double lr, double* h,
+                         double* g, double* pi, double* dh) {
+  double g2[64];
+  const double v2 = na_critic(n, t->phi2, g2);
+  const double v = na_critic(n, t->phi, g);
+  const double delta = t->r + gamma * v2 - v;
+  /* critic: θ += lr·δ·∂V(s)/∂θ */
+  for (int k = 0; k < n->H; ++k) {
+    const double back = n->u2[k] * (1.0 - g[k] * g[k]);
+    for (int f = 0; f < n->F; ++f) n->U1[k * n->F + f] += lr * delta * back * t->phi[f];
+    n->c1[k] += lr * delta * back;
+  }
+  for (int k = 0; k < n->H; ++k) n->u2[k] += lr * delta * g[k];
+  n->c2 += lr * delta;
+  /* actor: θ += lr·δ·∇ log π(a|s) */
+  na_actor(n, t->phi, t->avail, h, pi);
+  for (int k = 0; k < n->H; ++k) {
+    double s = 0.0;
+    for (int b = 0; b < n->A; ++b) {
+      if (!t->avail[b]) continue;
+      const double e = (b == t->a ? 1.0 : 0.0) - pi[b];
+      s += e * n->W2[b * n->H + k];
+    }
+    dh[k] = s * (1.0 - h[k] * h[k]);
+  }
+  for (int b = 0; b < n->A; ++b) {
+    if (!t->avail[b]) continue;
+    const double e = (b == t->a ? 1.0 : 0.0) - pi[b];
+    for (int k = 0; k < n->H; ++k) n->W2[b * n->H + k] += lr * delta * e * h[k];
+    n->b2[b] += lr * delta * e;
+  }
+  for (int k = 0; k < n->H; ++k) {
+    for (int f = 0; f < n->F; ++f) n->W1[k * n->F + f] += lr * delta * dh[k] * t->phi[f];
+    n->b1[k] += lr * delta * dh[k];
+  }
+}
+
+/* visited hashtable H_v: rank → cost (open addressing) */
+typedef struct {
+  uint64_t* key;
+  double* val;
+  unsigned char* used;
+  uint64_t cap;
+} na_map;
+
+static uint64_t na_slot(const na_map* m, uint64_t r) {
+  uint64_t h = (r * 0x9E3779B97F4A7C15ULL) % m->cap;
+  while (m->used[h] && m->key[h] != r) h = (h + 1) % m->cap;
+  return h;
+}
+
+static double na_reward(double cs, double cs2, double clip) {
+  if (isinf(cs2)) return isinf(cs) ? 0.0 : -clip;
+  if (isinf(cs)) return clip;
+  double r = log(cs / cs2);
+  if (r > clip) r = clip;
+  if (r < -clip) r = -clip;
+  return r;
+}
+
+int or_na2c(const or_space* sp, const or_config* s0, const or_na2c_params* prm,
+            int64_t budget, uint64_t seed, or_cost_fn cost, void* ctx, or_gbfs_result* res,
+            uint64_t* log_ranks, double* log_costs, int64_t log_cap) {
+  uint64_t size;
+  if (or_space_size(sp, &size) || !s0 || !prm || !cost || !res) return -1;
+  if (budget < 1 || prm->T < 1 || prm->B < 1 || prm->H < 1 || prm->H > 64 || prm->mem < 1 ||
+      prm->max_walks < 1 || !or_legit(sp, s0))
+    return -1;
+  tables tb;
+  build_tables(sp, &tb);
+  na_net n;
+  if (na_alloc(sp, prm, seed, &n)) return -1;
+  na_map hv;
+  hv.cap = (uint64_t)budget * 4 + 17;
+  hv.key = (uint64_t*)calloc(hv.cap, sizeof(uint64_t));
+  hv.val = (double*)calloc(hv.cap, sizeof(double));
+  hv.used = (unsigned char*)calloc(hv.cap, 1);
+  na_trans* mem = (na_trans*)calloc((size_t)prm->mem, sizeof(na_trans));
+  or_config* coll = (or_config*)calloc((size_t)prm->B, sizeof(or_config));
+  uint64_t* coll_r = (uint64_t*)calloc((size_t)prm->B, sizeof(uint64_t));
+  double h[64], g[64], dh[64], pi[3 * OR_MAXD * OR_MAXD + 1];
+  int64_t mem_n = 0, mem_head = 0; /* FIFO: oldest at mem_head */
+  uint64_t rng = seed;
+  int64_t timed = 0, episodes = 0;
+
+  uint64_t r0;
+  rank_with(sp, &tb, s0, &r0);
+  or_config c0cfg = *s0;
+  const double c0 = cost(&c0cfg, r0, ctx);
+  if (timed < log_cap) {
+    log_ranks[timed] = r0;
+    log_costs[timed] = c0;
+  }
+  ++timed;
+  {
+    const uint64_t sl = na_slot(&hv, r0);
+    hv.used[sl] = 1;
+    hv.key[sl] = r0;
+    hv.val[sl] = c0;
+  }
+  double cost_min = c0;
+  uint64_t best = r0;
+  or_config center = *s0;
+
+  while (timed < budget) {
+    /* collect B unvisited legitimate states by T-step walks from the centre */
+    int nb = 0;
+    for (int w = 0; w < prm->max_walks && nb < prm->B; ++w) {
+      or_config s = center;
+      for (int t = 0; t < prm->T; ++t) {
+        double phi[3 * OR_MAXD + 1];
+        int avail[3 * OR_MAXD * OR_MAXD + 1], navail = 0;
+        for (int a = 0; a < n.A; ++a) {
+          avail[a] = na_available(&n, &s, a);
+          navail += avail[a];
+        }
+        int a = -1;
+        if (na_uniform(&rng) < prm->eps) {
+          na_features(sp, &n, &s, phi);
+          na_actor(&n, phi, avail, h, pi);
+          const double u = na_uniform(&rng);
+          double cum = 0.0;
+          for (int b = 0; b < n.A; ++b) {
+            if (!avail[b]) continue;
+            a = b; /* the last available action if rounding leaves u ≥ Σπ */
+            cum += pi[b];
+            if (u < cum) break;
+          }
+        } else {
+          int k = (int)(or_splitmix64_next(&rng) % (uint64_t)navail);
+          for (int b = 0; b < n.A; ++b)
+            if (avail[b] && k-- == 0) {
+              a = b;
+              break;
+            }
+        }
+        const or_config s2 = na_step(&n, &s, a);
+        if (or_legit(sp, &s2)) {
+          uint64_t r2;
+          rank_with(sp, &tb, &s2, &r2);
+          int dup = hv.used[na_slot(&hv, r2)];
+          for (int b = 0; b < nb && !dup; ++b) dup = coll_r[b] == r2;
+          if (!dup && nb < prm->B) {
+            coll[nb] = s2;
+            coll_r[nb] = r2;
+            ++nb;
+          }
+        }
+        s = s2;
+      }
+    }
+    ++episodes;
+    if (nb == 0) break; /* the neighbourhood of the centre is exhausted */
+    for (int b = 0; b < nb && timed < budget; ++b) {
+      or_config sc = coll[b];
+      const double c = cost(&sc, coll_r[b], ctx);
+      if (timed < log_cap) {
+        log_ranks[timed] = coll_r[b];
+        log_costs[timed] = c;
+      }
+      ++timed;
+      if (c < cost_min) {
+        cost_min = c;
+        best = coll_r[b];
+        center = coll[b];
+      }
+      const uint64_t sl = na_slot(&hv, coll_r[b]);
+      hv.used[sl] = 1;
+      hv.key[sl] = coll_r[b];
+      hv.val[sl] = c;
+      /* every (s, a) with step(s, a) = s' and s already timed */
+      for (int bb = 0; bb < n.A; ++bb) {
+        if (!na_available(&n, &coll[b], bb)) continue;
+        const or_config p = na_step(&n, &coll[b], bb);
+        if (!or_member(sp, &p)) continue;
+        uint64_t rp;
+        rank_with(sp, &tb, &p, &rp);
+        const uint64_t ps = na_slot(&hv, rp);
+        if (!hv.used[ps]) continue;
+        na_trans tr;
+        memset(&tr, 0, sizeof(tr));
+        na_features(sp, &n, &p, tr.phi);
+        na_features(sp, &n, &coll[b], tr.phi2);
+        for (int a = 0; a < n.A; ++a) tr.avail[a] = na_available(&n, &p, a);
+        tr.a = na_inverse(&n, bb);
+        tr.r = na_reward(hv.val[ps], c, prm->r_clip);
+        if (mem_n < prm->mem) {
+          mem[(mem_head + mem_n) % prm->mem] = tr;
+          ++mem_n;
+        } else {
+          mem[mem_head] = tr;
+          mem_head = (mem_head + 1) % prm->mem;
+        }
+      }
+      /* one pass over M, oldest first */
+      for (int64_t k = 0; k < mem_n; ++k)
+        na_train_one(&n, &mem[(mem_head + k) % prm->mem], prm->gamma, prm->lr, h, g, pi, dh);
+    }
+  }
+  unrank_with(sp, &tb, best, &res->best);
+  res->best.legit = or_legit(sp, &res->best);
+  res->best_cost = cost_min;
+  res->timed = timed;
+  res->popped = episodes;
+  free(hv.key);
+  free(hv.val);
+  free(hv.used);
+  free(mem);
+  free(coll);
+  free(coll_r);
+  na_free(&n);
+  free_tables(&tb);
+  return 0;
+}
+
+int or_na2c_probe(const or_space* sp, const or_na2c_params* prm, uint64_t seed,
+                  const or_config* s, int a, const double* actor_params,
+                  const double* critic_params, double* pi, double* v,
+                  double* g_actor, double* g_critic, int64_t* n_actor, int64_t* n_critic) {
+  uint64_t size;
+  if (or_space_size(sp, &size) || !prm || prm->H < 1 || prm->H > 64) return -1;
+  na_net n;
+  if (na_alloc(sp, prm, seed, &n)) return -1;
+  const int F = n.F, A = n.A, H = n.H;
+  const int64_t na = (int64_t)H * F + H + (int64_t)A * H + A, nc = (int64_t)H * F + H + H + 1;
+  if (n_actor) *n_actor = na;
+  if (n_critic) *n_critic = nc;
+  if (!s || !pi || !v || !g_actor || !g_critic || a < 0 || a >= A) {
+    na_free(&n);
+    return 0;
+  }
+  if (actor_params) {
+    int64_t k = 0;
+    for (int t = 0; t < H * F; ++t) n.W1[t] = actor_params[k++];
+    for (int t = 0; t < H; ++t) n.b1[t] = actor_params[k++];
+    for (int t = 0; t < A * H; ++t) n.W2[t] = actor_params[k++];
+    for (int t = 0; t < A; ++t) n.b2[t] = actor_params[k++];
+  }
+  if (critic_params) {
+    int64_t k = 0;
+    for (int t = 0; t < H * F; ++t) n.U1[t] = critic_params[k++];
+    for (int t = 0; t < H; ++t) n.c1[t] = critic_params[k++];
+    for (int t = 0; t < H; ++t) n.u2[t] = critic_params[k++];
+    n.c2 = critic_params[k++];
+  }
+  double phi[3 * OR_MAXD + 1], h[64], g[64];
+  int avail[3 * OR_MAXD * OR_MAXD + 1];
+  na_features(sp, &n, s, phi);
+  for (int b = 0; b < A; ++b) avail[b] = na_available(&n, s, b);
+  na_actor(&n, phi, avail, h, pi);
+  *v = na_critic(&n, phi, g);
+  /* ∇ log π(a|s): the update direction na_train_one applies (δ = 1, lr = 1) */
+  int64_t k = 0;
+  double dh[64];
+  for (int q = 0; q < H; ++q) {
+    double sacc = 0.0;
+    for (int b = 0; b < A; ++b) {
+      if (!avail[b]) continue;
+      sacc += ((b == a ? 1.0 : 0.0) - pi[b]) * n.W2[b * H + q];
+    }
+    dh[q] = sacc * (1.0 - h[q] * h[q]);
+  }
+  for (int q = 0; q < H; ++q)
+    for (int f = 0; f < F; ++f) g_actor[k++] = dh[q] * phi[f];
+  for (int q = 0; q < H; ++q) g_actor[k++] = dh[q];
+  for (int b = 0; b < A; ++b)
+    for (int q = 0; q < H; ++q)
+      g_actor[k++] = avail[b] ? ((b == a ? 1.0 : 0.0) - pi[b]) * h[q] : 0.0;
+  for (int b = 0; b < A; ++b) g_actor[k++] = avail[b] ? (b == a ? 1.0 : 0.0) - pi[b] : 0.0;
+  k = 0;
+  for (int q = 0; q < H; ++q)
+    for (int f = 0; f < F; ++f) g_critic[k++] = n.u2[q] * (1.0 - g[q] * g[q]) * phi[f];
+  for (int q = 0; q < H; ++q) g_critic[k++] = n.u2[q] * (1.0 - g[q] * g[q]);
+  for (int q = 0; q < H; ++q) g_critic[k++] = g[q];
+  g_critic[k++] = 1.0;
+  na_free(&n);
+  return 0;
+}

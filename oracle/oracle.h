@@ -98,6 +98,36 @@ int or_random_search(const or_space* sp, int64_t budget, uint64_t seed, or_cost_
                      void* ctx, or_gbfs_result* res, uint64_t* log_ranks, double* log_costs,
                      int64_t log_cap);
 
+/* N-A2C (§4.3, Alg.2) with the readings listed with the library's
+ * implementation: action list (per dimension, ordered level pairs the mode
+ * allows, then the MFMA toggle), features e_i/E per level (+ MFMA bit),
+ * one-hidden-layer tanh actor (softmax over the available actions) and critic,
+ * ε = probability of following π, T-step walks from the current centre until
+ * B unvisited legitimate states are collected (at most max_walks walks), each
+ * timed state storing every transition from an already-timed neighbour into
+ * the FIFO memory M (reward log(cost(s)/cost(s')) clipped to ±r_clip), and one
+ * SGD pass over M after every timing (critic: semi-gradient TD(0); actor:
+ * δ·∇log π). Randomness: SplitMix64(seed) for the walk, SplitMix64(seed ^
+ * 0xA2C0A2C0A2C0A2C0) for the initial weights. res->popped holds the number of
+ * episodes. Returns 0, or -1 on a bad argument. */
+typedef struct {
+  int32_t T, B, H, mem, max_walks;
+  double eps, gamma, lr, r_clip;
+} or_na2c_params;
+int or_na2c(const or_space* sp, const or_config* s0, const or_na2c_params* prm,
+            int64_t budget, uint64_t seed, or_cost_fn cost, void* ctx, or_gbfs_result* res,
+            uint64_t* log_ranks, double* log_costs, int64_t log_cap);
+/* The actor's and critic's outputs and gradients at one state for the
+ * weights after or_na2c's initialisation (for gradient checks): pi[A],
+ * v, and the flattened gradients of log π(a|s) (actor) and V(s) (critic)
+ * with respect to every parameter, in the order W1, b1, W2, b2 (actor) and
+ * U1, c1, u2, c2 (critic). Returns the parameter counts through n_actor and
+ * n_critic when the buffers are NULL. */
+int or_na2c_probe(const or_space* sp, const or_na2c_params* prm, uint64_t seed,
+                  const or_config* s, int a, const double* actor_params,
+                  const double* critic_params, double* pi, double* v,
+                  double* g_actor, double* g_critic, int64_t* n_actor, int64_t* n_critic);
+
 #ifdef __cplusplus
 }
 #endif

@@ -1,0 +1,164 @@
+"""Pins of the oracle's N-A2C (§4.3, Alg.2) against facts outside its code:
+finite-difference gradients of both networks, the softmax's support, the
+walk's first steps recomputed from the SplitMix64 definition, the graph
+distance of every timed state from the states timed before it, the budget,
+uniqueness and s* rules, and convergence on a unimodal landscape."""
+import math
+from collections import deque
+
+import numpy as np
+import pytest
+
+
+def _space(orc, mode=None, mfma=False):
+    mode = orc.ANY_PAIR if mode is None else mode
+    return orc.Space(64, 32, 64, (3, 2, 3), "bf16" if mfma else "f32", mfma, mode=mode)
+
+
+def _available(sp, cfg):
+    """Action list in the reading's order and which actions are available."""
+    acts = []
+    for x, f in enumerate(cfg[:3]):
+        d = len(f)
+        for i in range(d):
+            for j in range(d):
+                if i != j and (sp.mode == 1 or abs(i - j) == 1):
+                    acts.append((x, i, j, f[j] % 2 == 0))
+    if sp.mfma_coord:
+        acts.append(("mfma", 0, 0, True))
+    return acts
+
+
+@pytest.mark.parametrize("mfma", [False, True])
+def test_gradients_match_finite_differences(orc, mfma):
+    sp = _space(orc, mfma=mfma)
+    cfg = ((4, 2, 8), (8, 8), (2, 4, 4), 16 if mfma else 0)
+    assert sp.member(cfg)
+    acts = _available(sp, cfg)
+    a = next(k for k, t in enumerate(acts) if t[3])
+    base = orc.na2c_probe(sp, cfg, a, seed=3, params={"H": 6})
+    rng = np.random.default_rng(0)
+    theta = rng.normal(0, 0.5, base["n_actor"])
+    phi = rng.normal(0, 0.5, base["n_critic"])
+    p0 = orc.na2c_probe(sp, cfg, a, seed=3, params={"H": 6}, actor=theta, critic=phi)
+    h = 1e-6
+    for k in range(base["n_actor"]):
+        tp, tm = theta.copy(), theta.copy()
+        tp[k] += h
+        tm[k] -= h
+        lp = math.log(orc.na2c_probe(sp, cfg, a, 3, {"H": 6}, tp, phi)["pi"][a])
+        lm = math.log(orc.na2c_probe(sp, cfg, a, 3, {"H": 6}, tm, phi)["pi"][a])
+        assert abs((lp - lm) / (2 * h) - p0["g_actor"][k]) <= 1e-6 * (1 + abs(p0["g_actor"][k])), k
+    for k in range(base["n_critic"]):
+        cp, cm = phi.copy(), phi.copy()
+        cp[k] += h
+        cm[k] -= h
+        vp = orc.na2c_probe(sp, cfg, a, 3, {"H": 6}, theta, cp)["v"]
+        vm = orc.na2c_probe(sp, cfg, a, 3, {"H": 6}, theta, cm)["v"]
+        assert abs((vp - vm) / (2 * h) - p0["g_critic"][k]) <= 1e-6 * (1 + abs(p0["g_critic"][k])), k
+
+
+def test_policy_support_is_the_available_actions(orc):
+    sp = _space(orc)
+    for cfg in [((64, 1, 1), (64, 1), (32, 1, 1), 0), ((1, 1, 64), (1, 64), (1, 1, 32), 0),
+                ((8, 8, 1), (8, 8), (4, 2, 4), 0)]:
+        acts = _available(sp, cfg)
+        pr = orc.na2c_probe(sp, cfg, next(k for k, t in enumerate(acts) if t[3]), seed=1)
+        pi = pr["pi"]
+        assert len(pi) == len(acts)
+        assert abs(pi.sum() - 1.0) < 1e-12
+        for k, t in enumerate(acts):
+            assert (pi[k] > 0) == t[3], (cfg, k)
+
+
+def _splitmix(state):
+    state = (state + 0x9E3779B97F4A7C15) & (2 ** 64 - 1)
+    z = state
+    z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & (2 ** 64 - 1)
+    z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & (2 ** 64 - 1)
+    return state, z ^ (z >> 31)
+
+
+def test_random_walk_first_episode_from_the_definition(orc):
+    """eps = 0: every step is a uniform pick among the available actions
+    (SplitMix64 mod their count, in list order), so the first episode's
+    collected states follow from the definition alone."""
+    sp = _space(orc)
+    s0 = sp.paper_s0()
+    prm = {"eps": 0.0, "B": 5, "T": 3}
+    res = orc.na2c(sp, s0, 6, 11, lambda c, r: 1.0, prm)
+    state = 11
+    want, seen = [], {sp.rank(s0)}
+    while len(want) < 5:
+        s = s0
+        for _ in range(3):
+            acts = _available(sp, s)
+            avail = [t for t in acts if t[3]]
+            state, _ = _splitmix(state)    # the ε draw (never below 0)
+            state, z2 = _splitmix(state)   # the action draw
+            x, i, j, _ = avail[z2 % len(avail)]
+            f = [list(t) for t in s[:3]]
+            f[x][i] *= 2
+            f[x][j] //= 2
+            s = (tuple(f[0]), tuple(f[1]), tuple(f[2]), s[3])
+            r = sp.rank(s)
+            if sp.legit(s) and r not in seen and len(want) < 5:
+                want.append(r)
+                seen.add(r)
+    assert res["log_ranks"][1:6] == want
+
+
+def _distances(orc, sp, src, limit):
+    """Graph distances (neighbour moves) from src, up to `limit`."""
+    dist = {sp.rank(src): 0}
+    dq = deque([src])
+    while dq:
+        s = dq.popleft()
+        ds = dist[sp.rank(s)]
+        if ds == limit:
+            continue
+        for t, _ in sp.neighbours(s):
+            r = sp.rank(t)
+            if r not in dist:
+                dist[r] = ds + 1
+                dq.append(t)
+    return dist
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_trajectory_rules(orc, seed):
+    """Budget, uniqueness and legitimacy of the timed states, s* = the first
+    minimum, and every timed state within T moves of a state timed before it
+    (the centre of its episode is one of them)."""
+    sp = _space(orc, mfma=True)
+    s0 = sp.paper_s0()
+    costs = {}
+
+    def cost(c, r):
+        costs.setdefault(r, 1.0 + ((r * 2654435761 + seed) % 997) / 997.0)
+        return costs[r]
+
+    T = 3
+    res = orc.na2c(sp, s0, 80, seed, cost, {"T": T, "B": 6})
+    log = res["log_ranks"]
+    assert res["timed"] == len(log) <= 80 and len(set(log)) == len(log)
+    assert all(sp.legit(sp.unrank(r)) for r in log)
+    i = min(range(len(log)), key=lambda t: (res["log_costs"][t], t))
+    assert sp.rank(res["best"]) == log[i] and res["best_cost"] == res["log_costs"][i]
+    for k in range(1, len(log)):
+        near = any(_distances(orc, sp, sp.unrank(p), T).get(log[k], T + 1) <= T for p in log[:k])
+        assert near, k
+
+
+def test_unimodal_landscape_reaches_the_target(orc):
+    sp = orc.Space(256, 256, 256, (3, 2, 3), "f32", False, mode=orc.ANY_PAIR)
+    target = ((16, 2, 8), (16, 16), (8, 2, 16), 0)
+    assert sp.legit(target)
+
+    def cost(c, r):
+        e = [math.log2(v) for t in c[:3] for v in t]
+        g = [math.log2(v) for t in target[:3] for v in t]
+        return 1.0 + sum(abs(a - b) for a, b in zip(e, g))
+
+    res = orc.na2c(sp, sp.paper_s0(), 600, 5, cost)
+    assert res["best"] == target and res["best_cost"] == 1.0
