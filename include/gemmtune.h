@@ -201,7 +201,7 @@ typedef struct gt_tune_result {
   uint64_t best_rank;
   double best_cost;      /* cost_min (ms in GPU mode) */
   int64_t timed;         /* configurations timed (≤ budget) */
-  int64_t popped;        /* G-BFS: queue pops; random search: draws */
+  int64_t popped;        /* G-BFS: queue pops; random search: draws; N-A2C: episodes */
   int64_t skipped_illegit;
   int64_t skipped_visited;
   int64_t failed;        /* timed with cost +inf */
@@ -234,6 +234,49 @@ int tune_gbfs(const gt_space* sp, const gt_tune_opts* opts, gt_cost_fn cost,
  * Same ownership and error behaviour as tune_gbfs. */
 int tune_random(const gt_space* sp, const gt_tune_opts* opts, gt_cost_fn cost,
                 void* ctx, gt_tune_result* out);
+
+/* ---- N-A2C (§4.3, Alg.2) ------------------------------------------------ */
+
+/* Settings of N-A2C. The paper fixes T = 3 (§5); the rest are readings of
+ * what it leaves open. */
+typedef struct gt_na2c_params {
+  int32_t T;          /* steps per walk (𝒯); default 3 */
+  int32_t B;          /* len(B_test): states collected and timed per episode; 8 */
+  int32_t H;          /* hidden tanh units of the actor and of the critic, ≤ 64; 32 */
+  int32_t mem;        /* capacity of the FIFO memory 𝓜 (transitions); 256 */
+  int32_t max_walks;  /* walks per episode before it is timed with fewer than B; 64 */
+  int32_t reserved;
+  double eps;         /* probability of following π (else a uniform action); 0.8 */
+  double gamma;       /* discount of the TD(0) advantage; 0.9 */
+  double lr;          /* SGD step of actor and critic; 0.01 */
+  double r_clip;      /* reward log(cost(s)/cost(s')) clipped to ±r_clip; 5 */
+} gt_na2c_params;
+
+/* Fills the defaults listed in gt_na2c_params. */
+int gt_na2c_params_init(gt_na2c_params* p);
+
+/* N-A2C over the space, timed exactly as tune_gbfs (GPU or callback; same
+ * opts: s0 (NULL: the paper's [D,1,…,1], MFMA 16), budget, t_max_s, seed,
+ * log, progress). Actions: per dimension the ordered level pairs the
+ * neighbour mode allows (×2 at one level, ÷2 at the other; available when the
+ * halved factor is even), then the MFMA toggle. State features: each level's
+ * share of its dimension's power-of-two exponent, plus the MFMA bit. Actor:
+ * one hidden tanh layer, softmax over the available actions; critic: one
+ * hidden tanh layer, linear output; weights U(±1/√fan_in) from
+ * SplitMix64(seed ^ 0xA2C0A2C0A2C0A2C0), biases 0. Each episode walks T steps
+ * from the centre (s0, then the best state so far) until B unvisited
+ * legitimate states are collected (illegitimate states may be walked
+ * through, never collected) or max_walks walks were made; with probability
+ * eps a step samples π, else a uniform available action (SplitMix64(seed)).
+ * An episode that collects nothing lengthens the walks by one step (the
+ * paper lets the exploration step grow), up to T + 8, after which the search
+ * stops (stop_reason 1); a new best state resets them to T. The collected states are timed in order; after each timing, every
+ * transition (s, a, r, s') into it from an already-timed neighbour s joins
+ * 𝓜 and one SGD pass over 𝓜 (oldest first) trains the critic (TD(0)) and
+ * the actor (δ·∇log π). out->popped counts episodes. params NULL: the defaults. Same ownership and
+ * error behaviour as tune_gbfs. */
+int tune_na2c(const gt_space* sp, const gt_tune_opts* opts, const gt_na2c_params* params,
+              gt_cost_fn cost, void* ctx, gt_tune_result* out);
 
 /* Thread-local message of the last failure. */
 const char* gt_last_error(void);

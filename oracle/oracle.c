@@ -859,12 +859,14 @@ int or_na2c(const or_space* sp, const or_config* s0, const or_na2c_params* prm,
   uint64_t best = r0;
   or_config center = *s0;
 
+  int steps = prm->T; /* walk length; grows while episodes collect nothing */
   while (timed < budget) {
-    /* collect B unvisited legitimate states by T-step walks from the centre */
+    /* collect B unvisited legitimate states by walks of `steps` steps from
+     * the centre */
     int nb = 0;
     for (int w = 0; w < prm->max_walks && nb < prm->B; ++w) {
       or_config s = center;
-      for (int t = 0; t < prm->T; ++t) {
+      for (int t = 0; t < steps; ++t) {
         double phi[3 * OR_MAXD + 1];
         int avail[3 * OR_MAXD * OR_MAXD + 1], navail = 0;
         for (int a = 0; a < n.A; ++a) {
@@ -907,7 +909,13 @@ int or_na2c(const or_space* sp, const or_config* s0, const or_na2c_params* prm,
       }
     }
     ++episodes;
-    if (nb == 0) break; /* the neighbourhood of the centre is exhausted */
+    if (nb == 0) {
+      /* nothing new within `steps` of the centre: walk one step further
+       * (§4.3 lets the exploration step grow), up to T + 8 */
+      if (steps >= prm->T + 8) break;
+      ++steps;
+      continue;
+    }
     for (int b = 0; b < nb && timed < budget; ++b) {
       or_config sc = coll[b];
       const double c = cost(&sc, coll_r[b], ctx);
@@ -920,6 +928,7 @@ int or_na2c(const or_space* sp, const or_config* s0, const or_na2c_params* prm,
         cost_min = c;
         best = coll_r[b];
         center = coll[b];
+        steps = prm->T; /* a new centre: back to T-step walks */
       }
       const uint64_t sl = na_slot(&hv, coll_r[b]);
       hv.used[sl] = 1;

@@ -103,7 +103,9 @@ int or_random_search(const or_space* sp, int64_t budget, uint64_t seed, or_cost_
  * allows, then the MFMA toggle), features e_i/E per level (+ MFMA bit),
  * one-hidden-layer tanh actor (softmax over the available actions) and critic,
  * ε = probability of following π, T-step walks from the current centre until
- * B unvisited legitimate states are collected (at most max_walks walks), each
+ * B unvisited legitimate states are collected (at most max_walks walks; an
+ * episode that collects nothing lengthens the walks by one step, up to T + 8,
+ * then the search stops; a new best resets them to T), each
  * timed state storing every transition from an already-timed neighbour into
  * the FIFO memory M (reward log(cost(s)/cost(s')) clipped to ±r_clip), and one
  * SGD pass over M after every timing (critic: semi-gradient TD(0); actor:

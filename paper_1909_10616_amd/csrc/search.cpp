@@ -11,6 +11,14 @@
 //
 // Random search: ranks drawn uniformly (SplitMix64 mod |ξ|), illegitimate
 // and repeated draws skipped without cost, at most 64·budget + 1024 draws.
+//
+// N-A2C (§4.3, Alg.2): episodes of T-step walks from a centre (the best state
+// so far) collect B unvisited legitimate states, chosen ε-greedily between a
+// small actor network's policy and uniform actions; the collected states are
+// timed, and every transition into a timed state from an already-timed
+// neighbour trains the actor and a critic (one SGD pass over a FIFO memory
+// after every timing). The arithmetic is written in a fixed order (no
+// contraction of multiply-adds) so that a run is reproducible bit for bit.
 #include <hip/hip_runtime.h>
 
 #include <chrono>
@@ -19,12 +27,15 @@
 #include <cstring>
 #include <queue>
 #include <string>
+#include <unordered_map>
 #include <unordered_set>
 #include <utility>
 #include <vector>
 
 #include "internal.h"
 #include "runtime.h"
+
+#pragma clang fp contract(off)
 
 namespace gt {
 namespace {
@@ -398,6 +409,366 @@ int tune_random(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn cost, void
       have = true;
     }
   }
+  t.finish(best);
+  return GT_OK;
+}
+
+
+int gt_na2c_params_init(gt_na2c_params* p) {
+  if (!p) {
+    gt::set_error("gt_na2c_params_init: null");
+    return GT_EINVAL;
+  }
+  std::memset(p, 0, sizeof(*p));
+  p->T = 3;
+  p->B = 8;
+  p->H = 32;
+  p->mem = 256;
+  p->max_walks = 64;
+  p->eps = 0.8;
+  p->gamma = 0.9;
+  p->lr = 0.01;
+  p->r_clip = 5.0;
+  return GT_OK;
+}
+
+}  // extern "C"
+
+namespace gt {
+namespace {
+
+// The fixed action list of N-A2C: per dimension (m, k, n) the ordered level
+// pairs (i, j) the neighbour mode allows — ×2 at level i, ÷2 at level j —
+// then the MFMA toggle when the space has that coordinate.
+struct Move {
+  int dim, up, down;
+  bool toggle;
+};
+
+class Agent {
+ public:
+  Agent(const Space& s, const gt_na2c_params& p, uint64_t seed) : s_(s), H_(p.H) {
+    for (int x = 0; x < 3; ++x)
+      for (int i = 0; i < s.dim[x].d; ++i)
+        for (int j = 0; j < s.dim[x].d; ++j)
+          if (i != j && (s.mode == GT_ANY_PAIR || i - j == 1 || j - i == 1))
+            moves_.push_back({x, i, j, false});
+    if (s.mfma_coord) moves_.push_back({0, 0, 0, true});
+    A_ = static_cast<int>(moves_.size());
+    F_ = s.dim[0].d + s.dim[1].d + s.dim[2].d + (s.mfma_coord ? 1 : 0);
+    W1_.assign(H_ * F_, 0.0);
+    b1_.assign(H_, 0.0);
+    W2_.assign(A_ * H_, 0.0);
+    b2_.assign(A_, 0.0);
+    U1_.assign(H_ * F_, 0.0);
+    c1_.assign(H_, 0.0);
+    u2_.assign(H_, 0.0);
+    uint64_t ws = seed ^ 0xA2C0A2C0A2C0A2C0ull;
+    const double bF = 1.0 / std::sqrt(static_cast<double>(F_));
+    const double bH = 1.0 / std::sqrt(static_cast<double>(H_));
+    for (double& w : W1_) w = (2.0 * uniform(&ws) - 1.0) * bF;
+    for (double& w : W2_) w = (2.0 * uniform(&ws) - 1.0) * bH;
+    for (double& w : U1_) w = (2.0 * uniform(&ws) - 1.0) * bF;
+    for (double& w : u2_) w = (2.0 * uniform(&ws) - 1.0) * bH;
+  }
+
+  static double uniform(uint64_t* st) {
+    return static_cast<double>(splitmix64(st) >> 11) * (1.0 / 9007199254740992.0);
+  }
+
+  int actions() const { return A_; }
+  int features() const { return F_; }
+
+  static int64_t* lv(gt_config& c, int x) { return x == 0 ? c.m : (x == 1 ? c.k : c.n); }
+  static const int64_t* lv(const gt_config& c, int x) { return x == 0 ? c.m : (x == 1 ? c.k : c.n); }
+
+  bool available(const gt_config& c, int a) const {
+    const Move& m = moves_[a];
+    return m.toggle || lv(c, m.dim)[m.down] % 2 == 0;
+  }
+  gt_config step(const gt_config& c, int a) const {
+    gt_config t = c;
+    const Move& m = moves_[a];
+    if (m.toggle) {
+      t.mfma = c.mfma == 16 ? 32 : 16;
+    } else {
+      lv(t, m.dim)[m.up] = lv(c, m.dim)[m.up] * 2;
+      lv(t, m.dim)[m.down] = lv(c, m.dim)[m.down] / 2;
+    }
+    return t;
+  }
+  int inverse(int a) const {
+    const Move& m = moves_[a];
+    if (m.toggle) return a;
+    for (int b = 0; b < A_; ++b)
+      if (!moves_[b].toggle && moves_[b].dim == m.dim && moves_[b].up == m.down &&
+          moves_[b].down == m.up)
+        return b;
+    return -1;
+  }
+  void features(const gt_config& c, double* phi) const {
+    int k = 0;
+    for (int x = 0; x < 3; ++x) {
+      const Dim& dm = s_.dim[x];
+      for (int i = 0; i < dm.d; ++i) {
+        int64_t v = i == 0 ? lv(c, x)[0] / dm.q : lv(c, x)[i];
+        int e = 0;
+        while (v > 1) {
+          v >>= 1;
+          ++e;
+        }
+        phi[k++] = dm.E ? static_cast<double>(e) / static_cast<double>(dm.E) : 0.0;
+      }
+    }
+    if (s_.mfma_coord) phi[k++] = c.mfma == 32 ? 1.0 : 0.0;
+  }
+
+  // π over the available actions (0 elsewhere); h = hidden activations.
+  void policy(const double* phi, const char* avail, double* h, double* pi) const {
+    for (int k = 0; k < H_; ++k) {
+      double z = b1_[k];
+      for (int f = 0; f < F_; ++f) z += W1_[k * F_ + f] * phi[f];
+      h[k] = std::tanh(z);
+    }
+    double zmax = -INFINITY;
+    for (int a = 0; a < A_; ++a) {
+      pi[a] = 0.0;
+      if (!avail[a]) continue;
+      double z = b2_[a];
+      for (int k = 0; k < H_; ++k) z += W2_[a * H_ + k] * h[k];
+      pi[a] = z;
+      if (z > zmax) zmax = z;
+    }
+    double sum = 0.0;
+    for (int a = 0; a < A_; ++a)
+      if (avail[a]) {
+        pi[a] = std::exp(pi[a] - zmax);
+        sum += pi[a];
+      }
+    for (int a = 0; a < A_; ++a)
+      if (avail[a]) pi[a] /= sum;
+  }
+
+  double value(const double* phi, double* g) const {
+    double v = c2_;
+    for (int k = 0; k < H_; ++k) {
+      double z = c1_[k];
+      for (int f = 0; f < F_; ++f) z += U1_[k * F_ + f] * phi[f];
+      g[k] = std::tanh(z);
+      v += u2_[k] * g[k];
+    }
+    return v;
+  }
+
+  struct Transition {
+    double phi[3 * GT_MAXD + 1], phi2[3 * GT_MAXD + 1];
+    char avail[kMaxNeighbours];
+    int a;
+    double r;
+  };
+
+  // TD(0) advantage δ = r + γV(s') − V(s); critic θ += lr·δ·∇V(s); actor
+  // θ += lr·δ·∇log π(a|s); all gradients at the weights before this update.
+  void train(const Transition& t, double gamma, double lr) {
+    double g[64], g2[64], h[64], dh[64], pi[kMaxNeighbours];
+    const double v2 = value(t.phi2, g2);
+    const double v = value(t.phi, g);
+    const double delta = t.r + gamma * v2 - v;
+    for (int k = 0; k < H_; ++k) {
+      const double back = u2_[k] * (1.0 - g[k] * g[k]);
+      for (int f = 0; f < F_; ++f) U1_[k * F_ + f] += lr * delta * back * t.phi[f];
+      c1_[k] += lr * delta * back;
+    }
+    for (int k = 0; k < H_; ++k) u2_[k] += lr * delta * g[k];
+    c2_ += lr * delta;
+    policy(t.phi, t.avail, h, pi);
+    for (int k = 0; k < H_; ++k) {
+      double acc = 0.0;
+      for (int b = 0; b < A_; ++b)
+        if (t.avail[b]) acc += ((b == t.a ? 1.0 : 0.0) - pi[b]) * W2_[b * H_ + k];
+      dh[k] = acc * (1.0 - h[k] * h[k]);
+    }
+    for (int b = 0; b < A_; ++b) {
+      if (!t.avail[b]) continue;
+      const double e = (b == t.a ? 1.0 : 0.0) - pi[b];
+      for (int k = 0; k < H_; ++k) W2_[b * H_ + k] += lr * delta * e * h[k];
+      b2_[b] += lr * delta * e;
+    }
+    for (int k = 0; k < H_; ++k) {
+      for (int f = 0; f < F_; ++f) W1_[k * F_ + f] += lr * delta * dh[k] * t.phi[f];
+      b1_[k] += lr * delta * dh[k];
+    }
+  }
+
+ private:
+  const Space& s_;
+  int H_, A_ = 0, F_ = 0;
+  std::vector<Move> moves_;
+  std::vector<double> W1_, b1_, W2_, b2_, U1_, c1_, u2_;
+  double c2_ = 0.0;
+};
+
+double reward(double before, double after, double clip) {
+  if (std::isinf(after)) return std::isinf(before) ? 0.0 : -clip;
+  if (std::isinf(before)) return clip;
+  return std::min(clip, std::max(-clip, std::log(before / after)));
+}
+
+}  // namespace
+}  // namespace gt
+
+extern "C" {
+
+int tune_na2c(const gt_space* sp, const gt_tune_opts* o, const gt_na2c_params* params,
+              gt_cost_fn cost, void* ctx, gt_tune_result* out) {
+  using namespace gt;
+  Tuner t;
+  if (int rc = t.init(sp, o, cost, ctx, out, "tune_na2c")) return rc;
+  gt_na2c_params p;
+  gt_na2c_params_init(&p);
+  if (params) p = *params;
+  if (p.T < 1 || p.B < 1 || p.H < 1 || p.H > 64 || p.mem < 1 || p.max_walks < 1 ||
+      !(p.eps >= 0.0 && p.eps <= 1.0) || !(p.lr >= 0.0) || !(p.r_clip > 0.0)) {
+    set_error("tune_na2c: parameters out of range (T, B, mem, max_walks >= 1; 1 <= H <= 64; "
+              "0 <= eps <= 1; lr >= 0; r_clip > 0)");
+    return GT_EINVAL;
+  }
+  const Space& s = t.s;
+  gt_config s0{};
+  if (o->s0) {
+    s0 = *o->s0;
+  } else {
+    s0.d_m = s.dim[0].d;
+    s0.d_k = s.dim[1].d;
+    s0.d_n = s.dim[2].d;
+    s0.m[0] = sp->M;
+    s0.k[0] = sp->K;
+    s0.n[0] = sp->N;
+    for (int i = 1; i < s0.d_m; ++i) s0.m[i] = 1;
+    for (int i = 1; i < s0.d_k; ++i) s0.k[i] = 1;
+    for (int i = 1; i < s0.d_n; ++i) s0.n[i] = 1;
+    s0.mfma = s.mfma_coord ? 16 : 0;
+  }
+  if (!is_member(s, s0) || !legit_of(s, s0)) {
+    set_error("tune_na2c: s0 is not a legitimate member of the space");
+    return is_member(s, s0) ? GT_EILLEGIT : GT_EDIMS;
+  }
+  if (int rc = t.prepare_gpu(sp, "tune_na2c")) return rc;
+
+  Agent agent(s, p, o->seed);
+  const int A = agent.actions();
+  std::unordered_map<uint64_t, double> hv;  // H_v: rank → cost
+  std::vector<Agent::Transition> mem;       // M, FIFO
+  size_t mem_head = 0;
+  uint64_t rng = o->seed;
+
+  const uint64_t r0 = rank_of(s, s0);
+  const double c0 = t.time_one(s0, r0);
+  hv[r0] = c0;
+  t.cost_min = c0;
+  uint64_t best = r0;
+  if (t.fatal()) return t.fail_fatal("tune_na2c", s0, best);
+  gt_config centre = s0;
+
+  out->stop_reason = 1;
+  std::vector<gt_config> coll;
+  std::vector<uint64_t> coll_r;
+  double phi[3 * GT_MAXD + 1], h[64], pi[kMaxNeighbours];
+  char avail[kMaxNeighbours];
+  int walk = p.T;  // walk length: grows by one after an episode that collects nothing
+  while (true) {
+    if (out->timed >= o->budget) {
+      out->stop_reason = 0;
+      break;
+    }
+    if (o->t_max_s > 0.0 && t.elapsed() >= o->t_max_s) {
+      out->stop_reason = 2;
+      break;
+    }
+    // collect B unvisited legitimate states by walks from the centre
+    coll.clear();
+    coll_r.clear();
+    for (int w = 0; w < p.max_walks && static_cast<int>(coll.size()) < p.B; ++w) {
+      gt_config cur = centre;
+      for (int step = 0; step < walk; ++step) {
+        int navail = 0;
+        for (int a = 0; a < A; ++a) navail += (avail[a] = agent.available(cur, a) ? 1 : 0);
+        int act = -1;
+        if (Agent::uniform(&rng) < p.eps) {
+          agent.features(cur, phi);
+          agent.policy(phi, avail, h, pi);
+          const double u = Agent::uniform(&rng);
+          double cum = 0.0;
+          for (int b = 0; b < A; ++b) {
+            if (!avail[b]) continue;
+            act = b;
+            cum += pi[b];
+            if (u < cum) break;
+          }
+        } else {
+          int k = static_cast<int>(splitmix64(&rng) % static_cast<uint64_t>(navail));
+          for (int b = 0; b < A && act < 0; ++b)
+            if (avail[b] && k-- == 0) act = b;
+        }
+        const gt_config nxt = agent.step(cur, act);
+        if (legit_of(s, nxt)) {
+          const uint64_t r = rank_of(s, nxt);
+          bool dup = hv.count(r) != 0;
+          for (uint64_t q : coll_r) dup = dup || q == r;
+          if (!dup && static_cast<int>(coll.size()) < p.B) {
+            coll.push_back(nxt);
+            coll_r.push_back(r);
+          }
+        }
+        cur = nxt;
+      }
+    }
+    ++out->popped;
+    if (coll.empty()) {
+      // nothing new within `walk` steps of the centre: look one step further
+      // (the exploration step may grow, §4.3), up to T + 8, then stop
+      if (walk >= p.T + 8) {
+        out->stop_reason = 1;
+        break;
+      }
+      ++walk;
+      continue;
+    }
+    for (size_t b = 0; b < coll.size() && out->timed < o->budget; ++b) {
+      const double c = t.time_one(coll[b], coll_r[b]);
+      if (t.fatal()) return t.fail_fatal("tune_na2c", coll[b], best);
+      if (c < t.cost_min) {
+        t.cost_min = c;
+        best = coll_r[b];
+        centre = coll[b];
+        walk = p.T;  // a new centre: back to T-step walks
+      }
+      hv[coll_r[b]] = c;
+      // every (s, a) with step(s, a) = s' and s already timed
+      for (int bb = 0; bb < A; ++bb) {
+        if (!agent.available(coll[b], bb)) continue;
+        const gt_config prev = agent.step(coll[b], bb);
+        if (!is_member(s, prev)) continue;
+        const auto it = hv.find(rank_of(s, prev));
+        if (it == hv.end()) continue;
+        Agent::Transition tr{};
+        agent.features(prev, tr.phi);
+        agent.features(coll[b], tr.phi2);
+        for (int a = 0; a < A; ++a) tr.avail[a] = agent.available(prev, a) ? 1 : 0;
+        tr.a = agent.inverse(bb);
+        tr.r = reward(it->second, c, p.r_clip);
+        if (mem.size() < static_cast<size_t>(p.mem)) {
+          mem.push_back(tr);
+        } else {
+          mem[mem_head] = tr;
+          mem_head = (mem_head + 1) % mem.size();
+        }
+      }
+      for (size_t k = 0; k < mem.size(); ++k)
+        agent.train(mem[(mem_head + k) % mem.size()], p.gamma, p.lr);
+    }
+  }
+  if (out->timed >= o->budget) out->stop_reason = 0;
   t.finish(best);
   return GT_OK;
 }

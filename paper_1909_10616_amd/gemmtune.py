@@ -71,6 +71,13 @@ class gt_tune_opts(ctypes.Structure):
                 ("progress_s", ctypes.c_double)]
 
 
+class gt_na2c_params(ctypes.Structure):
+    _fields_ = [("T", ctypes.c_int32), ("B", ctypes.c_int32), ("H", ctypes.c_int32),
+                ("mem", ctypes.c_int32), ("max_walks", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("eps", ctypes.c_double),
+                ("gamma", ctypes.c_double), ("lr", ctypes.c_double), ("r_clip", ctypes.c_double)]
+
+
 class gt_tune_result(ctypes.Structure):
     _fields_ = [("best", gt_config), ("best_rank", ctypes.c_uint64),
                 ("best_cost", ctypes.c_double), ("timed", ctypes.c_int64),
@@ -82,7 +89,8 @@ class gt_tune_result(ctypes.Structure):
 
 EXPORTS = ("gt_space_size", "enumerate_configs", "config_rank", "config_unrank", "config_legit",
            "neighbours", "gemm_run", "gt_measure", "gt_reference_gemm", "gt_compare",
-           "gt_lower", "gt_tune_opts_init", "tune_gbfs", "tune_random", "gt_last_error")
+           "gt_lower", "gt_tune_opts_init", "tune_gbfs", "tune_random", "gt_na2c_params_init",
+           "tune_na2c", "gt_last_error")
 
 _lib = None
 
@@ -116,6 +124,9 @@ def lib():
                             ctypes.POINTER(gt_tune_result)]
     L.tune_random.argtypes = [SP, ctypes.POINTER(gt_tune_opts), gt_cost_fn, P,
                               ctypes.POINTER(gt_tune_result)]
+    L.gt_na2c_params_init.argtypes = [ctypes.POINTER(gt_na2c_params)]
+    L.tune_na2c.argtypes = [SP, ctypes.POINTER(gt_tune_opts), ctypes.POINTER(gt_na2c_params),
+                            gt_cost_fn, P, ctypes.POINTER(gt_tune_result)]
     L.gt_last_error.restype = ctypes.c_char_p
     for name in EXPORTS:
         if name != "gt_last_error":
@@ -293,7 +304,8 @@ def gt_compare(C, R, stream=None) -> float:
 
 
 def _tune(entry, space: Space, budget: int, s0, rho, seed, runs, warmup, check, t_max_s,
-          max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream, progress_s=0.0) -> dict:
+          max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream, progress_s=0.0,
+          na2c=None) -> dict:
     L = lib()
     o = gt_tune_opts()
     _check(L.gt_tune_opts_init(ctypes.byref(o)), "gt_tune_opts_init")
@@ -321,8 +333,16 @@ def _tune(entry, space: Space, budget: int, s0, rho, seed, runs, warmup, check, 
         o.c_ref = c_ref.data_ptr() if c_ref is not None else None
         o.stream = _stream(stream)
     res = gt_tune_result()
-    _check(getattr(L, entry)(ctypes.byref(space.c), ctypes.byref(o), cb, None, ctypes.byref(res)),
-           entry)
+    if entry == "tune_na2c":
+        prm = gt_na2c_params()
+        _check(L.gt_na2c_params_init(ctypes.byref(prm)), "gt_na2c_params_init")
+        for k, v in (na2c or {}).items():
+            setattr(prm, k, v)
+        rc = L.tune_na2c(ctypes.byref(space.c), ctypes.byref(o), ctypes.byref(prm), cb, None,
+                         ctypes.byref(res))
+    else:
+        rc = getattr(L, entry)(ctypes.byref(space.c), ctypes.byref(o), cb, None, ctypes.byref(res))
+    _check(rc, entry)
     del keep
     n = int(res.timed)
     entries = [{"rank": int(log[i].rank), "cost_ms": log[i].cost_ms, "first_ms": log[i].first_ms,
@@ -332,7 +352,9 @@ def _tune(entry, space: Space, budget: int, s0, rho, seed, runs, warmup, check, 
             "best_cost": res.best_cost, "timed": n, "popped": int(res.popped),
             "skipped_illegit": int(res.skipped_illegit),
             "skipped_visited": int(res.skipped_visited), "failed": int(res.failed),
-            "wall_s": res.wall_s, "stop_reason": STOP.get(res.stop_reason, "?"),
+            "wall_s": res.wall_s,
+            "stop_reason": ("neighbourhood-exhausted" if entry == "tune_na2c" and res.stop_reason == 1
+                            else STOP.get(res.stop_reason, "?")),
             "log": entries}
 
 
@@ -356,6 +378,19 @@ def tune_random(space: Space, budget: int, seed: int = 0, runs: int = 10, warmup
     tune_gbfs, ``popped`` counts the draws."""
     return _tune("tune_random", space, budget, None, 1, seed, runs, warmup, check, t_max_s,
                  max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream, progress_s)
+
+
+def tune_na2c(space: Space, budget: int, s0=None, seed: int = 0, runs: int = 10,
+              warmup: int = 1, check: bool = True, t_max_s: float = 0.0,
+              max_run_ms: float = 250.0, abort_factor: float = 50.0, A=None, B=None, C=None,
+              c_ref=None, cost_fn=None, stream=None, progress_s: float = 0.0,
+              params=None) -> dict:
+    """N-A2C (§4.3, Alg.2); timing, log and result as tune_gbfs (``popped``
+    counts episodes). ``params``: overrides of gt_na2c_params (T, B, H, mem,
+    max_walks, eps, gamma, lr, r_clip)."""
+    return _tune("tune_na2c", space, budget, s0, 1, seed, runs, warmup, check, t_max_s,
+                 max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream, progress_s,
+                 na2c=params)
 
 
 def tflops(M, N, K, ms) -> float:

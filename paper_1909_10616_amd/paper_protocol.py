@@ -1,12 +1,13 @@
 """The paper's own tuning protocol (§5) on one MI355X.
 
   python -m paper_1909_10616_amd.paper_protocol [--sizes 512,1024,2048]
-      [--seeds 1] [--out FILE.json]
+      [--seeds 1] [--methods gbfs,na2c] [--out FILE.json]
 
 Perceptron layers Y = WᵀX (W: k×m, X: k×n, fp32, U[−1,1), seed 0), the
 space shape of §5 — d = (4, 2, 4), moves between any two levels (Eq.6) —
-the paper's start state s0 = [[m,1,1,1],[k,1],[n,1,1,1]], ρ = 5, and a
-budget of 0.1 % of the space (484, 900 and 1,590 timed configurations).
+the paper's start state s0 = [[m,1,1,1],[k,1],[n,1,1,1]], ρ = 5 (G-BFS) and
+𝒯 = 3 (N-A2C, other settings at the library's defaults), and a budget of
+0.1 % of the space (484, 900 and 1,590 timed configurations).
 Every candidate is timed by the library as in every other search (1 warm-up,
 mean of 10 runs, output checked against the reference). Reported per size
 and seed: best cost (ms, TFLOP/s, % of the fp32 MFMA peak), configurations
@@ -34,6 +35,7 @@ def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--sizes", default="512,1024,2048")
     ap.add_argument("--seeds", type=int, default=1)
+    ap.add_argument("--methods", default="gbfs")
     ap.add_argument("--out", default=None)
     args = ap.parse_args()
 
@@ -58,16 +60,23 @@ def main():
         torch.cuda.synchronize()
         sp = gt.Space(w.M, w.N, w.K, w.d, w.dtype, w.mfma_coord, mode=gt.ANY_PAIR, a_kmajor=True)
         s0 = ((w.M, 1, 1, 1), (w.K, 1), (w.N, 1, 1, 1), 0)
-        for seed in range(args.seeds):
-            print(f"{w.name} seed {seed}: G-BFS, budget {w.budget} of {sp.size()}", flush=True)
+        for method, seed in [(m, k) for k in range(args.seeds) for m in args.methods.split(",")]:
+            print(f"{w.name} seed {seed}: {method}, budget {w.budget} of {sp.size()}", flush=True)
             t = time.perf_counter()
-            r = gt.tune_gbfs(sp, budget=w.budget, s0=s0, rho=5, seed=seed, A=Wd, B=Xd, C=C,
-                             c_ref=R, progress_s=30.0)
+            if method == "gbfs":
+                r = gt.tune_gbfs(sp, budget=w.budget, s0=s0, rho=5, seed=seed, A=Wd, B=Xd, C=C,
+                                 c_ref=R, progress_s=30.0)
+            elif method == "na2c":
+                r = gt.tune_na2c(sp, w.budget, s0=s0, seed=seed, A=Wd, B=Xd, C=C, c_ref=R,
+                                 progress_s=30.0)
+            else:
+                raise SystemExit(f"unknown method {method!r}")
             wall = time.perf_counter() - t
             costs = [e["cost_ms"] for e in r["log"]]
             argmin = min(range(len(costs)), key=lambda i: (costs[i], i))
             consistent = r["log"][argmin]["rank"] == r["best_rank"]
-            row = {"workload": w.name, "M": w.M, "N": w.N, "K": w.K, "seed": seed,
+            row = {"workload": w.name, "method": method, "M": w.M, "N": w.N, "K": w.K,
+                   "seed": seed,
                    "space_size": sp.size(), "budget": w.budget, "timed": r["timed"],
                    "fraction_pct": 100.0 * r["timed"] / sp.size(),
                    "best": gt.fmt_cfg(r["best"]), "best_ms": r["best_cost"],
@@ -80,15 +89,15 @@ def main():
                    "best_is_log_argmin": consistent}
             row["pct_of_fp32_peak"] = round(100.0 * row["tflops"] / PEAK_F32, 2)
             rows.append(row)
-            print(f"{w.name} seed {seed}: {row['tflops']:.2f} TFLOP/s "
+            print(f"{w.name} seed {seed} {method}: {row['tflops']:.2f} TFLOP/s "
                   f"({row['pct_of_fp32_peak']} % of fp32 peak), best {row['best']}, "
                   f"s0 {row['s0_ms']:.2f} ms, {r['timed']} timed in {wall:.0f} s, "
                   f"s* = argmin of the log: {consistent}", flush=True)
     summary = {}
-    for name in sorted({r["workload"] for r in rows}):
-        v = [r["tflops"] for r in rows if r["workload"] == name]
-        summary[name] = {"seeds": len(v), "min": min(v), "median": statistics.median(v),
-                         "max": max(v)}
+    for name, method in sorted({(r["workload"], r["method"]) for r in rows}):
+        v = [r["tflops"] for r in rows if r["workload"] == name and r["method"] == method]
+        summary[f"{name} {method}"] = {"seeds": len(v), "min": min(v),
+                                       "median": statistics.median(v), "max": max(v)}
     print(json.dumps({"summary": summary}), flush=True)
     if args.out:
         with open(args.out, "w") as f:

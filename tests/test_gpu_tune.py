@@ -1,4 +1,4 @@
-"""G-BFS on the GPU (through the C ABI).
+"""G-BFS, random search and N-A2C on the GPU (through the C ABI).
 
 Timing noise means several trajectories are correct, so the checks are:
 the budget is respected, s* is the argmin of the timing log, no timed
@@ -95,6 +95,42 @@ def test_gpu_random_search_replays_in_oracle(gt, orc, case):
     os_ = orc.Space(M, N, K, d, dt, mc)
     table = {e["rank"]: e["cost_ms"] for e in log}
     rep = orc.random_search(os_, budget, 9, lambda c, r: table.get(r, math.inf))
+    assert rep["log_ranks"] == [e["rank"] for e in log]
+    assert rep["best"] == res["best"] and rep["best_cost"] == res["best_cost"]
+    gt.gemm_run(res["best"], Ad, Bd, C)
+    torch.cuda.synchronize()
+    ref = orc.gemm(raw_bytes(A), raw_bytes(B), M, N, K, dt)
+    err = np.abs(C.cpu().numpy().astype(np.float64) - ref).max() / np.abs(ref).max()
+    assert err <= (1e-5 * K ** 0.5 if dt == "f32" else 2e-3)
+
+
+NA2C_GPU_CASES = [
+    # (M, N, K, d, dtype, mfma_coord, mode, budget)
+    (256, 256, 256, (4, 2, 4), "f32", False, 1, 48),
+    (512, 512, 512, (4, 4, 4), "bf16", True, 0, 48),
+]
+
+
+@pytest.mark.parametrize("case", NA2C_GPU_CASES, ids=["f32-256-paper-space", "bf16-512"])
+def test_gpu_na2c_replays_in_oracle(gt, orc, case):
+    """N-A2C on the GPU from the paper's s0: every timed output matched the
+    reference, and the oracle's N-A2C fed the logged costs takes the
+    identical trajectory (walks, policy, training) and keeps the same s*."""
+    M, N, K, d, dt, mc, mode, budget = case
+    dev = torch.device("cuda:0")
+    A, B = make_inputs(M, N, K, dt, 2, "uniform" if dt == "f32" else "normal")
+    Ad, Bd = A.to(dev), B.to(dev)
+    C = torch.empty(M, N, device=dev)
+    sp = gt.Space(M, N, K, d, dt, mc, mode=mode)
+    os_ = orc.Space(M, N, K, d, dt, mc, mode=mode)
+    s0 = os_.paper_s0()
+    print(f"na2c {M}x{N}x{K} {dt} budget {budget}", flush=True)
+    res = gt.tune_na2c(sp, budget, s0=s0, seed=6, A=Ad, B=Bd, C=C)
+    log = res["log"]
+    assert res["timed"] == len(log) <= budget
+    assert all(e["status"] in ("ok", "early-abort") for e in log)
+    table = {e["rank"]: e["cost_ms"] for e in log}
+    rep = orc.na2c(os_, s0, budget, 6, lambda c, r: table.get(r, math.inf))
     assert rep["log_ranks"] == [e["rank"] for e in log]
     assert rep["best"] == res["best"] and rep["best_cost"] == res["best_cost"]
     gt.gemm_run(res["best"], Ad, Bd, C)

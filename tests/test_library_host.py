@@ -283,3 +283,53 @@ def test_tune_random_errors_and_time_limit(gt):
 
     r = gt.tune_random(ls, budget=10 ** 6, t_max_s=0.2, cost_fn=slow)
     assert r["stop_reason"] == "time-limit" and 1 <= r["timed"] < 200
+
+
+NA2C_CASES = [
+    # (M, N, K, d, dtype, mfma, mode, budget, seed, params)
+    (512, 512, 512, (4, 2, 4), "f32", False, 1, 300, 0, None),        # the paper's space shape
+    (1024, 1024, 1024, (4, 2, 4), "f32", False, 1, 300, 7, {"B": 4, "T": 2}),
+    (256, 256, 512, (4, 4, 4), "bf16", True, 0, 250, 3, {"eps": 0.5, "mem": 64}),
+    (96, 80, 48, (4, 3, 4), "bf16", True, 1, 200, 1, {"H": 8, "lr": 0.05}),
+    (64, 32, 64, (3, 2, 3), "f32", False, 1, 400, 2, None),           # small: walks lengthen
+]
+
+
+@pytest.mark.parametrize("cost_kind", ["random", "unimodal"])
+@pytest.mark.parametrize("case", NA2C_CASES, ids=[f"{c[0]}x{c[1]}x{c[2]}-{c[4]}-{i}"
+                                                  for i, c in enumerate(NA2C_CASES)])
+def test_tune_na2c_synthetic_trajectory_matches_oracle(gt, orc, case, cost_kind):
+    """The library's N-A2C and the oracle's, fed the same synthetic costs,
+    time the identical sequence of configurations (which exercises the walk,
+    the policy sampling, the memory and every training step bit for bit)."""
+    M, N, K, d, dt, mc, mode, budget, seed, params = case
+    sp = gt.Space(M, N, K, d, dt, mc, mode=mode)
+    osp = orc.Space(M, N, K, d, dt, mc, mode=mode)
+    s0 = osp.paper_s0()
+    if cost_kind == "random":
+        cost = lambda c, r: 1.0 + ((r * 2654435761 + seed) % 997) / 997.0   # noqa: E731
+    else:
+        tgt = [e // 2 for e in range(sum(d))]
+
+        def cost(c, r):
+            e = [v.bit_length() - 1 for t in c[:3] for v in t]
+            return 1.0 + sum(abs(a - b) for a, b in zip(e, tgt))
+    res = gt.tune_na2c(sp, budget, s0=s0, seed=seed, cost_fn=cost, params=params)
+    ref = orc.na2c(osp, s0, budget, seed, cost, params)
+    assert [e["rank"] for e in res["log"]] == ref["log_ranks"]
+    assert [e["cost_ms"] for e in res["log"]] == ref["log_costs"]
+    assert res["timed"] == ref["timed"] and res["popped"] == ref["popped"]
+    assert res["best"] == ref["best"] and res["best_cost"] == ref["best_cost"]
+
+
+def test_tune_na2c_errors(gt):
+    sp = gt.Space(256, 256, 256, (3, 3, 3), "f32", False)
+    for bad in ({"T": 0}, {"B": 0}, {"H": 65}, {"mem": 0}, {"max_walks": 0}, {"eps": 1.5},
+                {"lr": -1.0}, {"r_clip": 0.0}):
+        with pytest.raises(gt.GemmTuneError):
+            gt.tune_na2c(sp, 10, cost_fn=lambda c, r: 1.0, params=bad)
+    with pytest.raises(gt.GemmTuneError):   # s0 not in the space
+        gt.tune_na2c(sp, 10, s0=((128, 1, 1), (256, 1, 1), (256, 1, 1), 0),
+                     cost_fn=lambda c, r: 1.0)
+    r = gt.tune_na2c(sp, 1, cost_fn=lambda c, r: 1.0)   # default s0 = [D,1,1]
+    assert r["timed"] == 1 and r["best"] == ((256, 1, 1), (256, 1, 1), (256, 1, 1), 0)

@@ -128,8 +128,9 @@ def _distances(orc, sp, src, limit):
 @pytest.mark.parametrize("seed", [0, 1, 2])
 def test_trajectory_rules(orc, seed):
     """Budget, uniqueness and legitimacy of the timed states, s* = the first
-    minimum, and every timed state within T moves of a state timed before it
-    (the centre of its episode is one of them)."""
+    minimum, and every timed state within T + 8 moves of the best state timed
+    before it at some point (its episode's centre; walks grow from T to at
+    most T + 8 steps)."""
     sp = _space(orc, mfma=True)
     s0 = sp.paper_s0()
     costs = {}
@@ -140,14 +141,22 @@ def test_trajectory_rules(orc, seed):
 
     T = 3
     res = orc.na2c(sp, s0, 80, seed, cost, {"T": T, "B": 6})
+    T += 8  # walks lengthen by up to 8 steps after episodes that collect nothing
     log = res["log_ranks"]
     assert res["timed"] == len(log) <= 80 and len(set(log)) == len(log)
     assert all(sp.legit(sp.unrank(r)) for r in log)
     i = min(range(len(log)), key=lambda t: (res["log_costs"][t], t))
     assert sp.rank(res["best"]) == log[i] and res["best_cost"] == res["log_costs"][i]
+    # the centre of an episode is the best state timed before it: one of the
+    # running-minimum records of the log
+    costs_log = res["log_costs"]
+    records, dist = [], {}
     for k in range(1, len(log)):
-        near = any(_distances(orc, sp, sp.unrank(p), T).get(log[k], T + 1) <= T for p in log[:k])
-        assert near, k
+        j = k - 1
+        if not records or costs_log[j] < costs_log[records[-1]]:
+            records.append(j)
+            dist[j] = _distances(orc, sp, sp.unrank(log[j]), T)
+        assert any(dist[j].get(log[k], T + 1) <= T for j in records), k
 
 
 def test_unimodal_landscape_reaches_the_target(orc):
