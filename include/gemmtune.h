@@ -269,8 +269,9 @@ int gt_na2c_params_init(gt_na2c_params* p);
  * through, never collected) or max_walks walks were made; with probability
  * eps a step samples π, else a uniform available action (SplitMix64(seed)).
  * An episode that collects nothing lengthens the walks by one step (the
- * paper lets the exploration step grow), up to T + 8, after which the search
- * stops (stop_reason 1); a new best state resets them to T. The collected states are timed in order; after each timing, every
+ * paper lets the exploration step grow) and halves the share of policy steps,
+ * up to T + 8 steps, after which the search stops (stop_reason 1); a new best
+ * state resets both. The collected states are timed in order; after each timing, every
  * transition (s, a, r, s') into it from an already-timed neighbour s joins
  * 𝓜 and one SGD pass over 𝓜 (oldest first) trains the critic (TD(0)) and
  * the actor (δ·∇log π). out->popped counts episodes. params NULL: the defaults. Same ownership and

@@ -859,7 +859,8 @@ int or_na2c(const or_space* sp, const or_config* s0, const or_na2c_params* prm,
   uint64_t best = r0;
   or_config center = *s0;
 
-  int steps = prm->T; /* walk length; grows while episodes collect nothing */
+  int steps = prm->T;      /* walk length; grows while episodes collect nothing */
+  double eps_cur = prm->eps; /* share of policy steps; halves with each such episode */
   while (timed < budget) {
     /* collect B unvisited legitimate states by walks of `steps` steps from
      * the centre */
@@ -874,7 +875,7 @@ int or_na2c(const or_space* sp, const or_config* s0, const or_na2c_params* prm,
           navail += avail[a];
         }
         int a = -1;
-        if (na_uniform(&rng) < prm->eps) {
+        if (na_uniform(&rng) < eps_cur) {
           na_features(sp, &n, &s, phi);
           na_actor(&n, phi, avail, h, pi);
           const double u = na_uniform(&rng);
@@ -911,9 +912,11 @@ int or_na2c(const or_space* sp, const or_config* s0, const or_na2c_params* prm,
     ++episodes;
     if (nb == 0) {
       /* nothing new within `steps` of the centre: walk one step further
-       * (§4.3 lets the exploration step grow), up to T + 8 */
+       * (§4.3 lets the exploration step grow) and halve the share of policy
+       * steps, up to T + 8 */
       if (steps >= prm->T + 8) break;
       ++steps;
+      eps_cur *= 0.5;
       continue;
     }
     for (int b = 0; b < nb && timed < budget; ++b) {
@@ -928,7 +931,8 @@ int or_na2c(const or_space* sp, const or_config* s0, const or_na2c_params* prm,
         cost_min = c;
         best = coll_r[b];
         center = coll[b];
-        steps = prm->T; /* a new centre: back to T-step walks */
+        steps = prm->T; /* a new centre: back to T-step walks and ε */
+        eps_cur = prm->eps;
       }
       const uint64_t sl = na_slot(&hv, coll_r[b]);
       hv.used[sl] = 1;

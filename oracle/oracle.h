@@ -104,8 +104,9 @@ int or_random_search(const or_space* sp, int64_t budget, uint64_t seed, or_cost_
  * one-hidden-layer tanh actor (softmax over the available actions) and critic,
  * ε = probability of following π, T-step walks from the current centre until
  * B unvisited legitimate states are collected (at most max_walks walks; an
- * episode that collects nothing lengthens the walks by one step, up to T + 8,
- * then the search stops; a new best resets them to T), each
+ * episode that collects nothing lengthens the walks by one step and halves
+ * the share ε of policy steps, up to T + 8 steps, then the search stops; a
+ * new best resets both), each
  * timed state storing every transition from an already-timed neighbour into
  * the FIFO memory M (reward log(cost(s)/cost(s')) clipped to ±r_clip), and one
  * SGD pass over M after every timing (critic: semi-gradient TD(0); actor:

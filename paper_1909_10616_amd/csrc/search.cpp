@@ -675,7 +675,8 @@ int tune_na2c(const gt_space* sp, const gt_tune_opts* o, const gt_na2c_params* p
   std::vector<uint64_t> coll_r;
   double phi[3 * GT_MAXD + 1], h[64], pi[kMaxNeighbours];
   char avail[kMaxNeighbours];
-  int walk = p.T;  // walk length: grows by one after an episode that collects nothing
+  int walk = p.T;        // walk length: grows by one after an episode that collects nothing
+  double eps_now = p.eps;  // share of policy steps: halves after such an episode
   while (true) {
     if (out->timed >= o->budget) {
       out->stop_reason = 0;
@@ -694,7 +695,7 @@ int tune_na2c(const gt_space* sp, const gt_tune_opts* o, const gt_na2c_params* p
         int navail = 0;
         for (int a = 0; a < A; ++a) navail += (avail[a] = agent.available(cur, a) ? 1 : 0);
         int act = -1;
-        if (Agent::uniform(&rng) < p.eps) {
+        if (Agent::uniform(&rng) < eps_now) {
           agent.features(cur, phi);
           agent.policy(phi, avail, h, pi);
           const double u = Agent::uniform(&rng);
@@ -726,12 +727,14 @@ int tune_na2c(const gt_space* sp, const gt_tune_opts* o, const gt_na2c_params* p
     ++out->popped;
     if (coll.empty()) {
       // nothing new within `walk` steps of the centre: look one step further
-      // (the exploration step may grow, §4.3), up to T + 8, then stop
+      // (the exploration step may grow, §4.3) with half the policy steps,
+      // up to T + 8, then stop
       if (walk >= p.T + 8) {
         out->stop_reason = 1;
         break;
       }
       ++walk;
+      eps_now *= 0.5;
       continue;
     }
     for (size_t b = 0; b < coll.size() && out->timed < o->budget; ++b) {
@@ -741,7 +744,8 @@ int tune_na2c(const gt_space* sp, const gt_tune_opts* o, const gt_na2c_params* p
         t.cost_min = c;
         best = coll_r[b];
         centre = coll[b];
-        walk = p.T;  // a new centre: back to T-step walks
+        walk = p.T;  // a new centre: back to T-step walks and the full ε
+        eps_now = p.eps;
       }
       hv[coll_r[b]] = c;
       // every (s, a) with step(s, a) = s' and s already timed
