@@ -260,6 +260,11 @@ def main():
             # the fastest is the reported configuration
             ok = sorted((e["cost_ms"], e["rank"]) for e in res["log"] if e["status"] == "ok")
             ranks = [res["best_rank"]] + [r for _, r in ok if r != res["best_rank"]][:TOPK - 1]
+            # untimed warm-up: REPEAT launches of s* right after the search's
+            # many short runs, so that every re-timing starts from the same
+            # sustained-load state of the board
+            for _ in range(REPEAT):
+                gt.gemm_run(res["best"], Ad, Bd, C, stream=stream)
             top = []
             for r in ranks:
                 cfg = sp.unrank(r)
