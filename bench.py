@@ -332,6 +332,9 @@ def main():
             "search_best_config": fmt_cfg(last["search_best"]),
             "search_best_cost_ms": last["best_cost"], "best_ms": best_ms,
             "retimed_top_us": last["top"],
+            # internal consistency of the search (a 10-run cost against a
+            # 200-launch re-timing of the same s*)
+            "s_star_retime_within_5pct": abs(last["top"][0][1] * 1e-3 / last["best_cost"] - 1.0) <= 0.05,
             "search_wall_s": round(last["wall_s"], 2), "failed": last["failed"],
             "stop": last["stop_reason"], "best_rel_diff_vs_reference": rel,
             "kernel": {k: info[k] for k in ("I", "TM", "TN", "fast", "dl", "ring", "waves", "BM",

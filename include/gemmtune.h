@@ -160,7 +160,10 @@ int gt_lower(const gt_config* cfg, int64_t M, int64_t N, int64_t K, int dtype,
 /* ---- G-BFS (§4.2, Alg.1) ---------------------------------------------- */
 
 /* Per-timed-configuration log record. status: 0 ok, 1 early abort,
- * 2 launch failure (cost +inf), 3 output mismatch (cost +inf). */
+ * 2 launch failure (cost +inf), 3 output mismatch (cost +inf). cost_ms is
+ * the mean of the timed runs (§5); median, minimum and sample standard
+ * deviation of the individual runs beside it (an early abort: the warm-up
+ * time, deviation 0; a callback cost: the cost itself). */
 typedef struct gt_log_entry {
   uint64_t rank;
   double cost_ms;
@@ -168,6 +171,9 @@ typedef struct gt_log_entry {
   double rel_err;
   int32_t status;
   int32_t reserved;
+  double median_ms;
+  double min_ms;
+  double stdev_ms;
 } gt_log_entry;
 
 /* Synthetic cost (the CPU "fake backend"): returns the cost of cfg, +inf for

@@ -10,6 +10,7 @@
 #include <cstring>
 #include <mutex>
 #include <string>
+#include <vector>
 
 #include "aux_kernels.h"
 #include "gemm_kernel.hpp"
@@ -189,23 +190,30 @@ int compare_on_gpu(const void* C, const void* R, int64_t n, hipStream_t s, doubl
 
 int measure(const gt_config& c, const void* A, const void* B, void* C, int64_t M, int64_t N,
             int64_t K, int dtype, hipStream_t s, int warmup, int runs, double abort_ms,
-            double* mean_ms, double* first_ms, int* aborted) {
+            double* mean_ms, double* first_ms, int* aborted, RunStats* stats) {
   Lowered lw;
   if (int rc = lower(c, M, N, K, dtype, A, B, C, &lw)) return rc;
-  hipEvent_t ev[4];
+  if (warmup < 1) warmup = 1;
+  if (runs < 1) runs = 1;
+  // events: [0], [1] around the first warm-up launch; [2 + r] before timed
+  // run r and [2 + runs] after the last, so each run has its own duration
+  std::vector<hipEvent_t> ev(static_cast<size_t>(runs) + 3, nullptr);
+  auto destroy = [&]() {
+    for (auto& x : ev)
+      if (x) hipEventDestroy(x);
+  };
   for (auto& x : ev) {
     hipError_t e = hipEventCreate(&x);
-    if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+    if (e != hipSuccess) {
+      x = nullptr;
+      destroy();
+      return hip_fail(e, "hipEventCreate");
+    }
   }
-  auto destroy = [&]() {
-    for (auto& x : ev) hipEventDestroy(x);
-  };
   int rc = GT_OK;
   float first = 0.0f, total = 0.0f;
   *aborted = 0;
   hipError_t e;
-  if (warmup < 1) warmup = 1;
-  if (runs < 1) runs = 1;
   // first warm-up launch, timed on its own for the early-abort rule
   if ((e = hipEventRecord(ev[0], s)) != hipSuccess) {
     destroy();
@@ -226,6 +234,7 @@ int measure(const gt_config& c, const void* A, const void* B, void* C, int64_t M
   if (abort_ms > 0.0 && first > abort_ms) {
     *aborted = 1;
     *mean_ms = first;
+    if (stats) *stats = RunStats{first, first, 0.0};
     destroy();
     return GT_OK;
   }
@@ -235,19 +244,34 @@ int measure(const gt_config& c, const void* A, const void* B, void* C, int64_t M
       return rc;
     }
   hipEventRecord(ev[2], s);
-  for (int r = 0; r < runs; ++r)
+  for (int r = 0; r < runs; ++r) {
     if ((rc = launch_lowered(lw, s)) != GT_OK) {
       hipStreamSynchronize(s);
       destroy();
       return rc;
     }
-  hipEventRecord(ev[3], s);
-  if ((e = hipEventSynchronize(ev[3])) != hipSuccess) {
+    hipEventRecord(ev[3 + r], s);
+  }
+  if ((e = hipEventSynchronize(ev[2 + runs])) != hipSuccess) {
     destroy();
     return hip_fail(e, "timed runs");
   }
-  hipEventElapsedTime(&total, ev[2], ev[3]);
+  hipEventElapsedTime(&total, ev[2], ev[2 + runs]);
   *mean_ms = static_cast<double>(total) / runs;
+  if (stats) {
+    std::vector<double> d(static_cast<size_t>(runs));
+    for (int r = 0; r < runs; ++r) {
+      float ms = 0.0f;
+      hipEventElapsedTime(&ms, ev[2 + r], ev[3 + r]);
+      d[r] = ms;
+    }
+    double var = 0.0;
+    for (double x : d) var += (x - *mean_ms) * (x - *mean_ms);
+    std::sort(d.begin(), d.end());
+    stats->median_ms = runs % 2 ? d[runs / 2] : 0.5 * (d[runs / 2 - 1] + d[runs / 2]);
+    stats->min_ms = d[0];
+    stats->stdev_ms = runs > 1 ? std::sqrt(var / (runs - 1)) : 0.0;
+  }
   destroy();
   return GT_OK;
 }
@@ -275,7 +299,7 @@ int gt_measure(const gt_config* cfg, const void* A, const void* B, void* C, int6
     return GT_EINVAL;
   }
   return gt::measure(*cfg, A, B, C, M, N, K, dtype, static_cast<hipStream_t>(stream), warmup, runs,
-                     abort_ms, mean_ms, first_ms, aborted);
+                     abort_ms, mean_ms, first_ms, aborted, nullptr);
 }
 
 int gt_reference_gemm(const void* A, const void* B, void* C, int64_t M, int64_t N, int64_t K,

@@ -20,9 +20,14 @@ struct Lowered {
 int lower(const gt_config& c, int64_t M, int64_t N, int64_t K, int dtype, const void* A,
           const void* B, void* C, Lowered* out);
 int launch_lowered(const Lowered& lw, hipStream_t s);
+// Spread of the timed runs of one measurement (each run between its own pair
+// of events; the mean is first-to-last over the runs).
+struct RunStats {
+  double median_ms, min_ms, stdev_ms;
+};
 int measure(const gt_config& c, const void* A, const void* B, void* C, int64_t M, int64_t N,
             int64_t K, int dtype, hipStream_t s, int warmup, int runs, double abort_ms,
-            double* mean_ms, double* first_ms, int* aborted);
+            double* mean_ms, double* first_ms, int* aborted, RunStats* stats);
 int compare_on_gpu(const void* C, const void* R, int64_t n, hipStream_t s, double* rel);
 
 }  // namespace gt

@@ -78,9 +78,13 @@ double gpu_cost(GpuCtx& g, const gt_config& c, double cost_min, gt_log_entry* re
     abort_ms = std::min(abort_ms > 0.0 ? abort_ms : INFINITY, g.o->abort_factor * cost_min);
   double mean = 0.0, first = 0.0;
   int aborted = 0;
+  RunStats st{NAN, NAN, NAN};
   const int rc = measure(c, g.o->A, g.o->B, g.o->C, g.M, g.N, g.K, g.dtype, g.s, g.o->warmup,
-                         g.o->runs, abort_ms, &mean, &first, &aborted);
+                         g.o->runs, abort_ms, &mean, &first, &aborted, &st);
   rec->first_ms = first;
+  rec->median_ms = st.median_ms;
+  rec->min_ms = st.min_ms;
+  rec->stdev_ms = st.stdev_ms;
   rec->rel_err = NAN;
   if (rc != GT_OK) {
     // A failed launch (no kernel, bad shape) leaves the device usable; a
@@ -222,6 +226,8 @@ struct Tuner {
       rec.cost_ms = v;
       rec.first_ms = v;
       rec.rel_err = NAN;
+      rec.median_ms = rec.min_ms = v;
+      rec.stdev_ms = 0.0;
       rec.status = std::isinf(v) ? 2 : 0;
     } else {
       v = gpu_cost(g, c, cost_min, &rec);

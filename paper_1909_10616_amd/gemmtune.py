@@ -52,7 +52,9 @@ class gt_kernel_info(ctypes.Structure):
 class gt_log_entry(ctypes.Structure):
     _fields_ = [("rank", ctypes.c_uint64), ("cost_ms", ctypes.c_double),
                 ("first_ms", ctypes.c_double), ("rel_err", ctypes.c_double),
-                ("status", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("status", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("median_ms", ctypes.c_double), ("min_ms", ctypes.c_double),
+                ("stdev_ms", ctypes.c_double)]
 
 
 gt_cost_fn = ctypes.CFUNCTYPE(ctypes.c_double, ctypes.POINTER(gt_config), ctypes.c_uint64,
@@ -346,7 +348,9 @@ def _tune(entry, space: Space, budget: int, s0, rho, seed, runs, warmup, check, 
     del keep
     n = int(res.timed)
     entries = [{"rank": int(log[i].rank), "cost_ms": log[i].cost_ms, "first_ms": log[i].first_ms,
-                "rel_err": log[i].rel_err, "status": STATUS.get(log[i].status, str(log[i].status))}
+                "median_ms": log[i].median_ms, "min_ms": log[i].min_ms,
+                "stdev_ms": log[i].stdev_ms, "rel_err": log[i].rel_err,
+                "status": STATUS.get(log[i].status, str(log[i].status))}
                for i in range(min(n, budget))]
     return {"best": from_c(res.best), "best_rank": int(res.best_rank),
             "best_cost": res.best_cost, "timed": n, "popped": int(res.popped),

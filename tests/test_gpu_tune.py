@@ -50,6 +50,10 @@ def test_gpu_search_is_consistent_and_replays_in_oracle(gt, orc, case):
     assert res["timed"] == budget or res["stop_reason"] == "queue-empty"
     assert all(e["status"] in ("ok", "early-abort") for e in log), \
         [e for e in log if e["status"] not in ("ok", "early-abort")][:3]
+    for e in log:   # the per-run spread logged beside the mean (§5: mean of 10 runs)
+        if e["status"] == "ok":
+            assert 0.0 < e["min_ms"] <= e["median_ms"] and e["stdev_ms"] >= 0.0
+            assert e["min_ms"] <= e["cost_ms"] * (1 + 1e-9)
     costs = [e["cost_ms"] for e in log]
     i = min(range(len(costs)), key=lambda t: (costs[t], t))
     assert res["best_rank"] == log[i]["rank"] and res["best_cost"] == costs[i]
