@@ -117,6 +117,31 @@ def cpu_baseline(w, A, B, target_s: float):
                       f"{dt:.1f} s"}
 
 
+def device_info():
+    """Name, compute units and maximum shader clock of GPU 0 as rocminfo
+    reports them, and the dense bf16 / fp32 MFMA peaks they imply (4096 and
+    256 flop per clock per CU)."""
+    import subprocess
+    import torch
+    p = torch.cuda.get_device_properties(0)
+    out = {"name": p.name, "arch": getattr(p, "gcnArchName", ""), "cus": p.multi_processor_count}
+    try:
+        txt = subprocess.run(["rocminfo"], capture_output=True, text=True, timeout=30).stdout
+        agent = next(a for a in txt.split("*******") if "gfx950" in a and "Compute Unit" in a)
+        for line in agent.splitlines():
+            if "Max Clock Freq. (MHz)" in line:
+                out["max_sclk_mhz"] = int(line.split(":")[1].split()[0])
+            if line.strip().startswith("Compute Unit:"):
+                out["cus"] = int(line.split(":")[1].split()[0])
+    except Exception as e:  # rocminfo missing or unparsable: report what torch gives
+        out["rocminfo_error"] = str(e)[:200]
+    if "max_sclk_mhz" in out:
+        ghz = out["max_sclk_mhz"] / 1000.0
+        out["peak_bf16_tflops_at_max_sclk"] = round(out["cus"] * ghz * 4096 / 1000.0, 1)
+        out["peak_f32_tflops_at_max_sclk"] = round(out["cus"] * ghz * 256 / 1000.0, 1)
+    return out
+
+
 def library_enumeration(sp):
     """The library's full enumeration of the space with J (a1, a2), streamed
     in chunks through enumerate_configs."""
@@ -349,6 +374,7 @@ def main():
             "hbm_gbs_at_algorithmic_bytes": round(alg_bytes / (best_ms * 1e-3) / 1e9, 1),
         },
     }
+    out["device"] = device_info()
     if not args.no_enumeration:
         log("library enumeration of the space ...")
         out["library_enumeration"] = library_enumeration(sp)
