@@ -209,8 +209,8 @@ def main():
     args = ap.parse_args()
 
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for {args.gpus}); the multi-GPU layout is "
-              "described in DESIGN.md and not built.", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}); splitting the search's "
+              "candidates or the GEMM's grid over several GPUs is not built.", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -1,5 +1,5 @@
 #!/bin/bash
-# Profiles bench.py's tuned GEMM with rocprofv3 into OUT (default gpurun_out/prof):
+# Profiles bench.py's tuned GEMM with rocprofv3 into OUT (default ./profile_out):
 #   1. the whole bench step under --kernel-trace --stats (the search and the re-timed best);
 #   2. FETCH_SIZE, then WRITE_SIZE, on the best configuration replayed 20 times;
 #   3. the same two counters on a plain 1 GiB device copy (their byte scale);
@@ -8,7 +8,7 @@
 # Usage: profile_bench.sh [OUT] [extra bench.py arguments, e.g. --workload NAME]
 set -u
 ROOT=$(cd "$(dirname "$0")/.." && pwd)
-OUT=$(realpath -m "${1:-$ROOT/gpurun_out/prof}")
+OUT=$(realpath -m "${1:-$ROOT/profile_out}")
 shift || true
 export TMPDIR=/tmp
 mkdir -p "$OUT"
