@@ -246,11 +246,11 @@ int tune_random(const gt_space* sp, const gt_tune_opts* opts, gt_cost_fn cost,
 /* Settings of N-A2C. The paper fixes T = 3 (§5); the rest are readings of
  * what it leaves open. */
 typedef struct gt_na2c_params {
-  int32_t T;          /* steps per walk (𝒯); default 3 */
-  int32_t B;          /* len(B_test): states collected and timed per episode; 8 */
-  int32_t H;          /* hidden tanh units of the actor and of the critic, ≤ 64; 32 */
-  int32_t mem;        /* capacity of the FIFO memory 𝓜 (transitions); 256 */
-  int32_t max_walks;  /* walks per episode before it is timed with fewer than B; 64 */
+  int32_t T;          /* steps per walk (𝒯), 1..64; default 3 */
+  int32_t B;          /* len(B_test): states collected and timed per episode, ≤ 65536; 8 */
+  int32_t H;          /* hidden tanh units of the actor and of the critic, 1..64; 32 */
+  int32_t mem;        /* capacity of the FIFO memory 𝓜 (transitions), ≤ 65536; 256 */
+  int32_t max_walks;  /* walks per episode before it is timed with fewer than B, ≤ 2^20; 64 */
   int32_t reserved;
   double eps;         /* probability of following π (else a uniform action); 0.8 */
   double gamma;       /* discount of the TD(0) advantage; 0.9 */

@@ -25,6 +25,8 @@
 #include <cmath>
 #include <cstdio>
 #include <cstring>
+#include <exception>
+#include <new>
 #include <queue>
 #include <string>
 #include <unordered_map>
@@ -271,8 +273,8 @@ struct Tuner {
 
 extern "C" {
 
-int tune_gbfs(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn cost, void* ctx,
-              gt_tune_result* out) {
+static int tune_gbfs_impl(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn cost, void* ctx,
+                          gt_tune_result* out) {
   using namespace gt;
   Tuner t;
   if (int rc = t.init(sp, o, cost, ctx, out, "tune_gbfs")) return rc;
@@ -368,8 +370,8 @@ int tune_gbfs(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn cost, void* 
   return GT_OK;
 }
 
-int tune_random(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn cost, void* ctx,
-                gt_tune_result* out) {
+static int tune_random_impl(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn cost, void* ctx,
+                            gt_tune_result* out) {
   using namespace gt;
   Tuner t;
   if (int rc = t.init(sp, o, cost, ctx, out, "tune_random")) return rc;
@@ -625,18 +627,19 @@ double reward(double before, double after, double clip) {
 
 extern "C" {
 
-int tune_na2c(const gt_space* sp, const gt_tune_opts* o, const gt_na2c_params* params,
-              gt_cost_fn cost, void* ctx, gt_tune_result* out) {
+static int tune_na2c_impl(const gt_space* sp, const gt_tune_opts* o, const gt_na2c_params* params,
+                          gt_cost_fn cost, void* ctx, gt_tune_result* out) {
   using namespace gt;
   Tuner t;
   if (int rc = t.init(sp, o, cost, ctx, out, "tune_na2c")) return rc;
   gt_na2c_params p;
   gt_na2c_params_init(&p);
   if (params) p = *params;
-  if (p.T < 1 || p.B < 1 || p.H < 1 || p.H > 64 || p.mem < 1 || p.max_walks < 1 ||
+  if (p.T < 1 || p.T > 64 || p.B < 1 || p.B > 65536 || p.H < 1 || p.H > 64 || p.mem < 1 ||
+      p.mem > 65536 || p.max_walks < 1 || p.max_walks > (1 << 20) ||
       !(p.eps >= 0.0 && p.eps <= 1.0) || !(p.lr >= 0.0) || !(p.r_clip > 0.0)) {
-    set_error("tune_na2c: parameters out of range (T, B, mem, max_walks >= 1; 1 <= H <= 64; "
-              "0 <= eps <= 1; lr >= 0; r_clip > 0)");
+    set_error("tune_na2c: parameters out of range (1 <= T <= 64; 1 <= B, mem <= 65536; "
+              "1 <= max_walks <= 2^20; 1 <= H <= 64; 0 <= eps <= 1; lr >= 0; r_clip > 0)");
     return GT_EINVAL;
   }
   const Space& s = t.s;
@@ -781,6 +784,42 @@ int tune_na2c(const gt_space* sp, const gt_tune_opts* o, const gt_na2c_params* p
   if (out->timed >= o->budget) out->stop_reason = 0;
   t.finish(best);
   return GT_OK;
+}
+
+
+}  // extern "C"
+
+namespace {
+// The searches allocate host memory as they go (queue, visited set, memory of
+// transitions); no C++ exception crosses the C ABI.
+template <class F>
+int guarded(const char* who, F f) {
+  try {
+    return f();
+  } catch (const std::bad_alloc&) {
+    gt::set_error(std::string(who) + ": out of host memory");
+  } catch (const std::exception& e) {
+    gt::set_error(std::string(who) + ": " + e.what());
+  }
+  return GT_EINVAL;
+}
+}  // namespace
+
+extern "C" {
+
+int tune_gbfs(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn cost, void* ctx,
+              gt_tune_result* out) {
+  return guarded("tune_gbfs", [&] { return tune_gbfs_impl(sp, o, cost, ctx, out); });
+}
+
+int tune_random(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn cost, void* ctx,
+                gt_tune_result* out) {
+  return guarded("tune_random", [&] { return tune_random_impl(sp, o, cost, ctx, out); });
+}
+
+int tune_na2c(const gt_space* sp, const gt_tune_opts* o, const gt_na2c_params* params,
+              gt_cost_fn cost, void* ctx, gt_tune_result* out) {
+  return guarded("tune_na2c", [&] { return tune_na2c_impl(sp, o, params, cost, ctx, out); });
 }
 
 }  // extern "C"
