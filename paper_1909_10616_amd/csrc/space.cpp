@@ -7,6 +7,7 @@
 // compositions directly instead of materialising the list.
 #include <algorithm>
 #include <cstring>
+#include <exception>
 #include <mutex>
 #include <thread>
 #include <vector>
@@ -287,11 +288,19 @@ void enumerate_range(const Space& s, uint64_t start, uint64_t n, gt_config* out)
   }
   std::vector<std::thread> th;
   const uint64_t chunk = (n + nt - 1) / nt;
-  for (unsigned t = 0; t < nt; ++t) {
-    const uint64_t a = t * chunk;
-    if (a >= n) break;
-    th.emplace_back(part, start + a, std::min(chunk, n - a));
+  uint64_t done = 0;  // records [0, done) are owned by started threads
+  try {
+    th.reserve(nt);
+    for (unsigned t = 0; t < nt; ++t) {
+      const uint64_t a = t * chunk;
+      if (a >= n) break;
+      th.emplace_back(part, start + a, std::min(chunk, n - a));
+      done = std::min(n, a + chunk);
+    }
+  } catch (const std::exception&) {
+    // no more threads: this thread fills the rest
   }
+  if (done < n) part(start + done, n - done);
   for (auto& t : th) t.join();
 }
 
