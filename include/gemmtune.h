@@ -258,7 +258,8 @@ typedef struct gt_na2c_params {
   double r_clip;      /* reward log(cost(s)/cost(s')) clipped to ±r_clip; 5 */
 } gt_na2c_params;
 
-/* Fills the defaults listed in gt_na2c_params. */
+/* Fills the defaults listed in gt_na2c_params (§5 fixes T = 3; the rest are
+ * the library's readings of §4.3). p: caller-owned. GT_EINVAL if p is NULL. */
 int gt_na2c_params_init(gt_na2c_params* p);
 
 /* N-A2C over the space, timed exactly as tune_gbfs (GPU or callback; same
