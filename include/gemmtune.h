@@ -216,7 +216,8 @@ typedef struct gt_tune_result {
   int32_t reserved;
 } gt_tune_result;
 
-/* Fills the defaults listed in gt_tune_opts (budget 1000, seed 0). */
+/* Fills the defaults listed in gt_tune_opts (budget 1000, seed 0).
+ * opts: caller-owned. GT_EINVAL if opts is NULL. */
 int gt_tune_opts_init(gt_tune_opts* opts);
 
 /* G-BFS over the space. cost == NULL times gemm_run on the GPU with
