@@ -1,0 +1,63 @@
+"""Host-side pieces of bench.py: the one-GPU guard, the kernel naming and
+launch signature the profiles are keyed by, and the traffic lookup that
+must only answer for the current kernel sources."""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def bench():
+    sys.path.insert(0, ROOT)
+    import bench as b
+    from paper_1909_10616_amd import gemmtune
+    if not os.path.exists(gemmtune.LIB_PATH):
+        import __graft_entry__
+        __graft_entry__.build()
+    return b
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2 and "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_signature_and_traffic_lookup(bench, tmp_path, monkeypatch):
+    from paper_1909_10616_amd import gemmtune as gt
+    from workloads import WORKLOADS
+    w = WORKLOADS["gemm4096_bf16"]
+    cfg = ((16, 2, 1, 128), (128, 1, 1, 32), (16, 4, 1, 64), 16)
+    info = gt.lower(cfg, w.M, w.N, w.K, w.dtype)
+    assert bench.kernel_name(w, info) == "gt::gemm_kernel_dl<16, 8, 4, 4>"
+    sig = bench.launch_signature(w, info)
+    assert sig == ("gemm4096_bf16 gt::gemm_kernel_dl<16,8,4,4> grid=256x1 waves=8 "
+                   "lds=163840 dl=1/5")
+    # a private profiles/traffic.txt: the line counts only with the current source hash
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    src = bench.kernel_source_hash()
+    (prof / "traffic.txt").write_text(
+        "# comment | not a record\n"
+        f"{sig} | source=0000000000000000 traffic_bytes=1\n"
+        f"{sig} | source={src} traffic_bytes=268905035\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: src)
+    assert bench.measured_traffic(w, info) == 268905035
+    (prof / "traffic.txt").write_text(f"{sig} | source=0000000000000000 traffic_bytes=1\n")
+    assert bench.measured_traffic(w, info) is None
+    other = dict(info, grid_y=2)
+    (prof / "traffic.txt").write_text(f"{sig} | source={src} traffic_bytes=5\n")
+    assert bench.measured_traffic(w, other) is None
+
+
+def test_committed_traffic_line_matches_the_sources(bench):
+    """profiles/traffic.txt holds a line for the bench's usual winner under the
+    kernel sources in the tree (it is refreshed whenever they change)."""
+    lines = [l for l in open(os.path.join(ROOT, "profiles", "traffic.txt"))
+             if not l.startswith("#") and "|" in l]
+    assert any(f"source={bench.kernel_source_hash()}" in l for l in lines)
