@@ -333,3 +333,16 @@ def test_tune_na2c_errors(gt):
                      cost_fn=lambda c, r: 1.0)
     r = gt.tune_na2c(sp, 1, cost_fn=lambda c, r: 1.0)   # default s0 = [D,1,1]
     assert r["timed"] == 1 and r["best"] == ((256, 1, 1), (256, 1, 1), (256, 1, 1), 0)
+
+
+@pytest.mark.parametrize("name", ["gemm2048_f32", "gemm4096_bf16", "mlp4096x11008x4096_bf16",
+                                  "skinny64x4096x4096_bf16", "paper1024_d424", "paper2048_d424"])
+def test_full_enumeration_every_workload_space(gt, orc, name):
+    """Every configuration of the remaining workload spaces (up to
+    188,392,750), library against oracle, in windows of 2^22."""
+    args = dict(SPACES)[name]
+    size = gt.Space(*args).size()
+    legit = 0
+    for start in range(0, size, 1 << 22):
+        legit += _compare_window(gt, orc, args, start, min(1 << 22, size - start))
+    assert 0 < legit < size
