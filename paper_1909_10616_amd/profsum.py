@@ -157,8 +157,12 @@ def report(out, copy_bytes=1 << 30):
     L.append(f"Launch: `{c['launch_signature']}`, kernel sources `{c['kernel_source']}`.")
     if last:
         r0 = last[-1]
-        L.append(f"Registers per lane: {r0.get('VGPR_Count')} VGPR + {r0.get('Accum_VGPR_Count')} AGPR, "
-                 f"{r0.get('SGPR_Count')} SGPR; scratch {r0.get('Scratch_Size')} B.")
+        vg = r0.get('VGPR_Count')
+        L.append(f"Registers per lane (kernel trace fields): VGPR_Count {vg}, Accum_VGPR_Count "
+                 f"{r0.get('Accum_VGPR_Count')}, SGPR_Count {r0.get('SGPR_Count')}; scratch "
+                 f"{r0.get('Scratch_Size')} B. The trace counts the descriptor's VGPR allocation "
+                 f"granules as 4 registers each; gfx950 allocates 8 per granule, so the wavefront "
+                 f"holds {2 * int(vg) if str(vg).isdigit() else '2x that'} VGPRs.")
     L.append("")
     L.append("## Kernel trace vs. bench timing")
     L.append("")
