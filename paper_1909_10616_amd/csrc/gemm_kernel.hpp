@@ -684,19 +684,33 @@ __device__ __forceinline__ void waitcnt_lgkm0() {
   __builtin_amdgcn_s_waitcnt(0xf | (0x3 << 14) | (0x7 << 4));  // lgkmcnt(0) only
 }
 
+// s_waitcnt takes its count as an immediate: wait for the largest of
+// {0, 1, 2, 3, 4, 6, 8, 12, 16, 24, 32, 48} that is at most n (a uniform
+// value), chosen by a balanced comparison tree.
 __device__ __forceinline__ void wait_vm_at_most(int n) {
-  if (n >= 48) waitcnt_vm<48>();
-  else if (n >= 32) waitcnt_vm<32>();
-  else if (n >= 24) waitcnt_vm<24>();
-  else if (n >= 16) waitcnt_vm<16>();
-  else if (n >= 12) waitcnt_vm<12>();
-  else if (n >= 8) waitcnt_vm<8>();
-  else if (n >= 6) waitcnt_vm<6>();
-  else if (n >= 4) waitcnt_vm<4>();
-  else if (n >= 3) waitcnt_vm<3>();
-  else if (n >= 2) waitcnt_vm<2>();
-  else if (n >= 1) waitcnt_vm<1>();
-  else waitcnt_vm<0>();
+  if (n >= 12) {
+    if (n >= 24) {
+      if (n >= 48) waitcnt_vm<48>();
+      else if (n >= 32) waitcnt_vm<32>();
+      else waitcnt_vm<24>();
+    } else {
+      if (n >= 16) waitcnt_vm<16>();
+      else waitcnt_vm<12>();
+    }
+  } else if (n >= 4) {
+    if (n >= 8) waitcnt_vm<8>();
+    else if (n >= 6) waitcnt_vm<6>();
+    else waitcnt_vm<4>();
+  } else {
+    if (n >= 2) {
+      if (n >= 3) waitcnt_vm<3>();
+      else waitcnt_vm<2>();
+    } else if (n >= 1) {
+      waitcnt_vm<1>();
+    } else {
+      waitcnt_vm<0>();
+    }
+  }
 }
 
 // One 16-byte-per-lane direct global→LDS load: lane j reads 16 bytes at
@@ -791,6 +805,10 @@ __device__ __forceinline__ void gemm_fast_dl(const KArgs& a, char* smem) {
     }
   }
   const int lds0 = __builtin_amdgcn_readfirstlane(static_cast<int>(lds_off(lds)));
+  const uint32_t stage16 = static_cast<uint32_t>(stage) * 16u;  // bytes per ring slot
+  // bytes between the A (B) origins of consecutive stages of this split-K slice
+  const uint64_t stepA = static_cast<uint64_t>(a.kSplit) * static_cast<uint64_t>(BK) * 2u;
+  const uint64_t stepB = stepA * static_cast<uint64_t>(a.N);
   // Instruction i (< ninst) of this wavefront for stage l into ring slot
   // `slot`; ga, gb: the stage's A and B origins as uniform scalars.
   // A or B is picked with scalar selects, not branches.
@@ -941,14 +959,17 @@ __device__ __forceinline__ void gemm_fast_dl(const KArgs& a, char* smem) {
     }
     load_frags(lds, 0, 0);
     // One stage; OPEN: both windows it touches are open (all but the last ns stages).
-    auto stage_step = [&](int l, auto open) __attribute__((always_inline)) {
+    // cur = l mod ns and its LDS byte address cur_b, and the global origins
+    // (ga2, gb2) of stage l + ns, are carried from stage to stage.
+    auto stage_step = [&](int l, int cur, uint32_t cur_b, uint64_t ga2, uint64_t gb2,
+                          auto open) __attribute__((always_inline)) {
       constexpr bool OPEN = decltype(open)::value;
-      const int cur = l % ns;
-      const u32x4* as = lds + cur * stage;
+      const u32x4* as = reinterpret_cast<const u32x4*>(smem + (cur_b - lds0));
       const int ld = l + ns - 1;  // stage whose window ends with this stage's boundary
       const bool load = OPEN || ld < a.kLoop;
       StageBase sbs{0, 0, 0};
-      if (load && NCS > 1) sbs = stage_base(ld, ld % ns);
+      if (load && NCS > 1)  // stage l + ns − 1 goes into slot (cur − 1) mod ns
+        sbs = StageBase{ga2 - stepA, gb2 - stepB, cur == 0 ? lds0 + (ns - 1) * stage16 : cur_b - stage16};
 #pragma unroll
       for (int cs = 0; cs + 1 < NCS; ++cs) {
         load_frags(as, cs + 1, (cs + 1) & 1);
@@ -959,10 +980,12 @@ __device__ __forceinline__ void gemm_fast_dl(const KArgs& a, char* smem) {
         }
       }
       const bool more = OPEN || l + 1 < a.kLoop;
-      const u32x4* nx = lds + ((l + 1) % ns) * stage;
+      const uint32_t nx_b = cur + 1 == ns ? lds0 : cur_b + stage16;
+      const u32x4* nx = reinterpret_cast<const u32x4*>(smem + (nx_b - lds0));
       if (more) {
         // stages issued after stage l + 1: l + 2 … min(l + ns − 1, kLoop − 1)
-        wait_vm_at_most(__builtin_amdgcn_readfirstlane(min(ns - 2, a.kLoop - 2 - l) * ninst));
+        const int pending = OPEN ? ns - 2 : min(ns - 2, a.kLoop - 2 - l);
+        wait_vm_at_most(__builtin_amdgcn_readfirstlane(pending * ninst));
         waitcnt_lgkm0();  // this wavefront's reads of slot cur are complete
         // every wavefront: stage l + 1 landed, done reading slot cur
         __builtin_amdgcn_s_barrier();
@@ -971,7 +994,7 @@ __device__ __forceinline__ void gemm_fast_dl(const KArgs& a, char* smem) {
       // last chunk-step; its slots open the window of stage l + ns (into slot cur)
       const bool load2 = OPEN || l + ns < a.kLoop;
       StageBase sb2{0, 0, 0};
-      if (load2) sb2 = stage_base(l + ns, cur);
+      if (load2) sb2 = StageBase{ga2, gb2, cur_b};
 #pragma unroll
       for (int q = 0; q < TMTN; ++q) {
         mfma1((NCS - 1) & 1, q);
@@ -981,9 +1004,32 @@ __device__ __forceinline__ void gemm_fast_dl(const KArgs& a, char* smem) {
         if (more) load_frags(nx, 0, 0);
       }
     };
-    int l = 0;
-    for (; l + ns < a.kLoop; ++l) stage_step(l, std::true_type{});
-    for (; l < a.kLoop; ++l) stage_step(l, std::false_type{});
+    int l = 0, cur = 0;
+    uint32_t cur_b = static_cast<uint32_t>(lds0);
+    // origins of stage ns (as integers: stage ns may lie past the end of K,
+    // then only stage ns − 1 = ga2 − stepA is ever loaded from them)
+    const uint64_t zA = static_cast<uint64_t>(z) * static_cast<uint64_t>(BK) * 2u;
+    uint64_t ga2 = uniform_ptr(Ag) + zA + static_cast<uint64_t>(ns) * stepA;
+    uint64_t gb2 = uniform_ptr(Bg) + zA * static_cast<uint64_t>(a.N) + static_cast<uint64_t>(ns) * stepB;
+    auto advance = [&]() __attribute__((always_inline)) {
+      ++l;
+      ga2 += stepA;
+      gb2 += stepB;
+      if (++cur == ns) {
+        cur = 0;
+        cur_b = static_cast<uint32_t>(lds0);
+      } else {
+        cur_b += stage16;
+      }
+    };
+    while (l + ns < a.kLoop) {
+      stage_step(l, cur, cur_b, ga2, gb2, std::true_type{});
+      advance();
+    }
+    while (l < a.kLoop) {
+      stage_step(l, cur, cur_b, ga2, gb2, std::false_type{});
+      advance();
+    }
   };
   if (ninst == kMaxDlInst)
     run(std::integral_constant<int, kMaxDlInst>{});
