@@ -417,3 +417,41 @@ def _replay_with_wait_slack(TMTN, NCS, cap, ninst, ns, kLoop, slack):
     ns_ = {}
     exec(compile(tree, "<ring>", "exec"), globals(), ns_)
     return ns_["ring_schedule"](TMTN, NCS, cap, ninst, ns, kLoop)
+
+
+@pytest.mark.parametrize("ns", range(2, 9))
+def test_ring_carried_state_matches_closed_forms(ns):
+    """The direct-load loop carries the ring slot, its LDS byte address and the
+    global byte origins of stage l + ns from stage to stage (slot + 1 with a
+    wrap, origins + one stage's stride) instead of computing them from l. The
+    same recurrences, replayed here, equal the closed forms for every stage:
+    slot l mod ns, origin ((l·kSplit + z)·BK) bytes of A and that times N of B,
+    the previous slot for stage l + ns − 1 and the next slot for stage l + 1."""
+    lds0, stage16, BK, N = 4096, 32768, 32, 4096
+    for kLoop in list(range(1, 21)) + [128]:
+        for kSplit in (1, 4):
+            for z in {0, kSplit - 1}:
+                stepA = kSplit * BK * 2
+                stepB = stepA * N
+                zA = z * BK * 2
+                cur, cur_b = 0, lds0
+                ga2, gb2 = zA + ns * stepA, zA * N + ns * stepB
+                for l in range(kLoop):
+                    assert cur == l % ns and cur_b == lds0 + (l % ns) * stage16
+                    assert ga2 == ((l + ns) * kSplit + z) * BK * 2
+                    assert gb2 == ((l + ns) * kSplit + z) * BK * 2 * N
+                    # stage l + ns − 1 (the first chunk-steps' window)
+                    prev_b = lds0 + (ns - 1) * stage16 if cur == 0 else cur_b - stage16
+                    assert prev_b == lds0 + ((l + ns - 1) % ns) * stage16
+                    assert ga2 - stepA == ((l + ns - 1) * kSplit + z) * BK * 2
+                    assert gb2 - stepB == ((l + ns - 1) * kSplit + z) * BK * 2 * N
+                    # stage l + 1 (the next fragments)
+                    nx_b = lds0 if cur + 1 == ns else cur_b + stage16
+                    assert nx_b == lds0 + ((l + 1) % ns) * stage16
+                    ga2 += stepA
+                    gb2 += stepB
+                    cur += 1
+                    if cur == ns:
+                        cur, cur_b = 0, lds0
+                    else:
+                        cur_b += stage16
