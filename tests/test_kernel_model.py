@@ -18,7 +18,9 @@ lane, that
 * in the direct-load ring, each (stage, load) pair is issued exactly once,
   never for a stage past kLoop, into a slot whose previous stage every
   wavefront has finished reading (a barrier in between), and is complete
-  (the vmcnt wait before a barrier) before any wavefront reads the stage.
+  (the vmcnt wait before a barrier) before any wavefront reads the stage;
+* the ring slot, its LDS address and the stage origins that the direct-load
+  loop carries from stage to stage equal their closed forms.
 
 The model restates the kernels' index formulas; it shares no code with them.
 """
