@@ -62,10 +62,11 @@ def kernel_name(w, info):
 
 
 def kernel_source_hash():
-    """Fingerprint of the sources that determine the GEMM kernels' code."""
+    """Fingerprint of the sources that hold the GPU kernels' code (how a
+    configuration lowers is part of the launch signature)."""
     import hashlib
     h = hashlib.sha256()
-    for f in ("gemm_kernel.hpp", "runtime.cpp", "gemm_inst.hip"):
+    for f in ("gemm_kernel.hpp", "gemm_inst.hip", "aux_kernels.hip"):
         with open(os.path.join(ROOT, "paper_1909_10616_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -94,27 +95,69 @@ def measured_traffic(w, info):
     return None
 
 
+def host_info():
+    """The host the CPU baseline runs on: logical CPUs, the CPUs this process
+    may use, and the CPU model."""
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), "")
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "affinity_cpus": len(os.sched_getaffinity(0)),
+            "cpu_model": model}
+
+
+def cpu_threads():
+    """Threads for the oracle: the CPU share the job is given (OMP_NUM_THREADS
+    when set, which the GPU machine sets to its per-GPU share), else every CPU
+    this process may use."""
+    aff = len(os.sched_getaffinity(0))
+    return max(1, min(int(os.environ.get("OMP_NUM_THREADS", "0")) or aff, aff))
+
+
 def cpu_baseline(w, A, B, target_s: float):
-    """The oracle (plain fp64 three-loop GEMM) on host cores, on a bounded
-    sample of rows of the same product, in TFLOP/s."""
+    """The oracle (plain fp64 three-loop GEMM) on host cores, in TFLOP/s: the
+    whole product when a 64-row sample says it fits in target_s, otherwise
+    that many rows. Returns the record and the product (None for a sample)."""
     import oracle
     from workloads import raw_bytes
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
-    threads = max(1, min(threads, 16, len(os.sched_getaffinity(0))))
+    threads = cpu_threads()
     Bb = raw_bytes(B)
     rows = min(w.M, 64)
     t = time.perf_counter()
     oracle.gemm(raw_bytes(A[:rows]), Bb, rows, w.N, w.K, w.dtype, nthreads=threads)
     cal = time.perf_counter() - t
-    rows = int(min(w.M, max(rows, rows * target_s / max(cal, 1e-3))))
-    rows = max(threads, rows - rows % threads)
+    est_full = cal * w.M / rows
+    if est_full <= target_s:
+        rows = w.M
+    else:
+        rows = int(min(w.M, max(rows, rows * target_s / max(cal, 1e-3))))
+        rows = max(threads, rows - rows % threads)
     t = time.perf_counter()
-    oracle.gemm(raw_bytes(A[:rows]), Bb, rows, w.N, w.K, w.dtype, nthreads=threads)
+    C = oracle.gemm(raw_bytes(A[:rows]), Bb, rows, w.N, w.K, w.dtype, nthreads=threads)
     dt = time.perf_counter() - t
     flops = 2.0 * rows * w.N * w.K
-    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
-            "sample": f"rows 0..{rows - 1} of C ({rows}x{w.N}x{w.K}, fp64 three-loop), "
-                      f"{dt:.1f} s"}
+    what = "all rows" if rows == w.M else f"rows 0..{rows - 1}"
+    rec = {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+           "sample": f"{what} of C ({rows}x{w.N}x{w.K}, fp64 three-loop, {threads} threads), "
+                     f"{dt:.1f} s", "host": host_info()}
+    return rec, (C if rows == w.M else None)
+
+
+def single_core_oracle():
+    """The oracle on one core at the two small workload shapes (256³ and
+    1024³ fp32): seconds and GFLOP/s per core."""
+    import oracle
+    from workloads import make_inputs, raw_bytes
+    out = {}
+    for n in (256, 1024):
+        A, B = make_inputs(n, n, n, "f32", 0, "uniform")
+        t = time.perf_counter()
+        oracle.gemm(raw_bytes(A), raw_bytes(B), n, n, n, "f32", nthreads=1)
+        dt = time.perf_counter() - t
+        out[f"{n}^3_f32"] = {"seconds": round(dt, 3), "gflops_per_core": round(2.0 * n ** 3 / dt / 1e9, 3)}
+    return out
 
 
 def device_info():
@@ -198,7 +241,7 @@ def main():
     ap.add_argument("--mode", choices=["adjacent", "any"], default="adjacent")
     ap.add_argument("--no-enumeration", action="store_true",
                     help="skip the timed full enumeration of the space")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=20.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--log-out", default=None, help="write the search log (JSON) here")
     ap.add_argument("--replay", default=None,
@@ -324,13 +367,25 @@ def main():
 
     last = results[-1]
     best_ms = last["best_ms"]
-    value = gt.tflops(w.M, w.N, w.K, best_ms)
     info = gt.lower(last["best"], w.M, w.N, w.K, w.dtype)
     peak = PEAK[w.dtype]
-    # correctness of s* against the GPU reference (the oracle checks live in tests/)
+    fig = gt.report(w.M, w.N, w.K, w.dtype, best_ms, last["timed"], size, peak)
+    value = fig["tflops"]
+    # C holds the reported configuration's output (its last re-timing)
     rel = gt.gt_compare(C, Cref, stream=stream)
-    esz = 2 if w.dtype == "bf16" else 4
-    alg_bytes = (w.M * w.K + w.K * w.N) * esz + w.M * w.N * 4
+    C_host = C.cpu().numpy()
+    alg_bytes = fig["algorithmic_bytes"]
+    # where a search's wall time goes: timing the candidates (their device
+    # time, then launch, wait and check overhead) and the host's own steps
+    # between candidates (neighbours, sampling, queue, lowering)
+    timed_n = max(last["timed"], 1)
+    search_split = {
+        "wall_s": round(last["wall_s"], 3), "eval_s": round(last["eval_s"], 3),
+        "device_s": round(last["device_s"], 3),
+        "host_between_candidates_us": round((last["wall_s"] - last["eval_s"]) / timed_n * 1e6, 1),
+        "eval_overhead_us": round((last["eval_s"] - last["device_s"]) / timed_n * 1e6, 1),
+        "device_share": round(last["device_s"] / max(last["wall_s"], 1e-9), 4),
+    }
 
     out = {
         "metric": METRIC,
@@ -351,9 +406,9 @@ def main():
             "levels_mkn": list(w.d), "mfma_coordinate": w.mfma_coord, "neighbours": args.mode,
             "rho": args.rho, "search_seed": args.seed, "s0": fmt_cfg(s0), "s0_kind": args.s0,
             "budget": budget, "configs_timed": last["timed"], "space_size": size,
-            "fraction_of_space_pct": 100.0 * last["timed"] / size,
+            "fraction_of_space_pct": fig["fraction_of_space_pct"],
             "best_config": fmt_cfg(last["best"]), "best_rank": last["best_rank"],
-            "pct_of_peak": round(100.0 * value / peak, 2),
+            "pct_of_peak": round(fig["pct_of_peak"], 2),
             "search_best_config": fmt_cfg(last["search_best"]),
             "search_best_cost_ms": last["best_cost"], "best_ms": best_ms,
             "retimed_top_us": last["top"],
@@ -362,6 +417,7 @@ def main():
             "s_star_retime_within_5pct": abs(last["top"][0][1] * 1e-3 / last["best_cost"] - 1.0) <= 0.05,
             "search_wall_s": round(last["wall_s"], 2), "failed": last["failed"],
             "stop": last["stop_reason"], "best_rel_diff_vs_reference": rel,
+            "search_time_split": search_split,
             "kernel": {k: info[k] for k in ("I", "TM", "TN", "fast", "dl", "ring", "waves", "BM",
                                             "BN", "BK", "dbuf", "lds_bytes", "grid_x", "grid_y")},
             "kernel_name": kernel_name(w, info), "launch_signature": launch_signature(w, info),
@@ -371,7 +427,7 @@ def main():
             "bound": "mfma", "achieved": round(value, 2), "peak": peak, "unit": "TFLOP/s",
             "frac": round(value / peak, 4), "traffic": measured_traffic(w, info),
             "algorithmic_bytes": alg_bytes,
-            "hbm_gbs_at_algorithmic_bytes": round(alg_bytes / (best_ms * 1e-3) / 1e9, 1),
+            "hbm_gbs_at_algorithmic_bytes": round(fig["hbm_gbs"], 1),
         },
     }
     out["device"] = device_info()
@@ -383,8 +439,16 @@ def main():
             json.dump({"config": out["config"], "log": last["log"]}, f)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
-        out["cpu_baseline"] = cpu_baseline(w, A, B, args.cpu_seconds)
-        log("oracle enumeration and G-BFS replay ...")
+        out["cpu_baseline"], C_oracle = cpu_baseline(w, A, B, args.cpu_seconds)
+        if C_oracle is not None:
+            # the reported configuration's whole output against the fp64 oracle
+            err = float(np.abs(C_host.astype(np.float64) - C_oracle).max() / np.abs(C_oracle).max())
+            out["rel_err_vs_oracle"] = err
+            out["rel_err_tolerance"] = 2e-3 if w.dtype == "bf16" else 1e-5 * math.sqrt(w.K)
+            out["matches_oracle"] = err <= out["rel_err_tolerance"]
+            del C_oracle
+        log("oracle single-core figures, enumeration and G-BFS replay ...")
+        out["cpu_baseline"]["single_core"] = single_core_oracle()
         out["cpu_baseline"].update(oracle_side(w, args.mode, s0, last, args.rho, args.seed))
     print(json.dumps(out), flush=True)
 

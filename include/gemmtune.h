@@ -10,8 +10,12 @@
  *   - Return value: GT_OK (0) or a negative gt_status; gt_last_error() gives a
  *     thread-local message for the last failure on the calling thread.
  *   - The caller owns every buffer passed in (host and device). The library
- *     owns only its kernel attribute cache and the per-search scratch it
- *     allocates when the caller passes none (freed before tune_gbfs returns).
+ *     owns (a) one 2-word device buffer per GPU for the output comparison
+ *     (gt_compare and the searches' checks), allocated on its first use on
+ *     that GPU and kept until gt_shutdown(), and (b) the M·N fp32 reference
+ *     product of a search whose caller passes no c_ref (freed before the
+ *     search returns). Kernel attributes (the dynamic LDS limit) are set once
+ *     per kernel and hold no memory.
  *   - Space functions (gt_space_size … neighbours) are pure host code, need no
  *     GPU and are thread-safe.
  *   - Dimension order is m, k, n everywhere, as in the paper's configuration
@@ -101,7 +105,8 @@ int config_unrank(const gt_space* sp, uint64_t rank, gt_config* cfg);
  * hardware predicate — waves ≤ 16; accumulator registers
  * acc = TM·TN·I²/64 ≤ 256 and acc + 96 ≤ 512/⌈waves/4⌉; LDS stage
  * (BM·BK + BK·BN)·sizeof(in) ≤ 163840 B; grid_M·grid_N·64·waves ≤ 2^32 − 1;
- * kSplit ≤ 65535. A non-member gives *J = 0 and GT_OK. */
+ * kSplit ≤ 65535; the whole launch grid_M·grid_N·kSplit·64·waves ≤ 2^32 − 1
+ * work-items. A non-member gives *J = 0 and GT_OK. */
 int config_legit(const gt_space* sp, const gt_config* cfg, int* J);
 
 /* Neighbour list g(s) = [step(s, a) for a in A] (§4.1 Eq.6, Eq.7, Eq.9) in
@@ -200,6 +205,11 @@ typedef struct gt_tune_opts {
   gt_log_entry* log;     /* optional, caller-owned, log_cap entries */
   int64_t log_cap;
   double progress_s;     /* > 0: a progress line on stderr at most this often */
+  int32_t trace_fd;      /* ≥ 0: before timing a candidate, one line naming it
+                            (index, rank, factors) is written to this file
+                            descriptor with write(2), so that the candidate
+                            in flight is on record if the process dies; -1 none */
+  int32_t reserved2;
 } gt_tune_opts;
 
 typedef struct gt_tune_result {
@@ -214,9 +224,13 @@ typedef struct gt_tune_result {
   double wall_s;
   int32_t stop_reason;   /* 0 budget, 1 queue empty, 2 time limit, 3 draws exhausted */
   int32_t reserved;
+  double eval_s;         /* wall time spent timing candidates (launches, waits,
+                            output checks; callback time in callback mode) */
+  double device_s;       /* GPU time of the timed launches as the events
+                            measured them (warm-ups included); 0 with a callback */
 } gt_tune_result;
 
-/* Fills the defaults listed in gt_tune_opts (budget 1000, seed 0).
+/* Fills the defaults listed in gt_tune_opts (budget 1000, seed 0, trace_fd -1).
  * opts: caller-owned. GT_EINVAL if opts is NULL. */
 int gt_tune_opts_init(gt_tune_opts* opts);
 
@@ -244,19 +258,23 @@ int tune_random(const gt_space* sp, const gt_tune_opts* opts, gt_cost_fn cost,
 
 /* ---- N-A2C (§4.3, Alg.2) ------------------------------------------------ */
 
-/* Settings of N-A2C. The paper fixes T = 3 (§5); the rest are readings of
- * what it leaves open. */
+/* Settings of N-A2C. The paper fixes T = 3 (§5) and the reward (§4.1); the
+ * rest are readings of what it leaves open. */
 typedef struct gt_na2c_params {
   int32_t T;          /* steps per walk (𝒯), 1..64; default 3 */
   int32_t B;          /* len(B_test): states collected and timed per episode, ≤ 65536; 8 */
   int32_t H;          /* hidden tanh units of the actor and of the critic, 1..64; 32 */
   int32_t mem;        /* capacity of the FIFO memory 𝓜 (transitions), ≤ 65536; 256 */
   int32_t max_walks;  /* walks per episode before it is timed with fewer than B, ≤ 2^20; 64 */
+  int32_t reward;     /* 0: r(s, a) = 1/cost(s') (§4.1, default); 1: variant
+                         log(cost(s)/cost(s')) clipped to ±r_clip */
+  int32_t eps_halving; /* 1: variant that also halves eps after an episode that
+                          collects nothing; 0 (default): eps stays fixed */
   int32_t reserved;
   double eps;         /* probability of following π (else a uniform action); 0.8 */
   double gamma;       /* discount of the TD(0) advantage; 0.9 */
   double lr;          /* SGD step of actor and critic; 0.01 */
-  double r_clip;      /* reward log(cost(s)/cost(s')) clipped to ±r_clip; 5 */
+  double r_clip;      /* clip of the log-ratio reward variant; 5 */
 } gt_na2c_params;
 
 /* Fills the defaults listed in gt_na2c_params (§5 fixes T = 3; the rest are
@@ -277,15 +295,26 @@ int gt_na2c_params_init(gt_na2c_params* p);
  * through, never collected) or max_walks walks were made; with probability
  * eps a step samples π, else a uniform available action (SplitMix64(seed)).
  * An episode that collects nothing lengthens the walks by one step (the
- * paper lets the exploration step grow) and halves the share of policy steps,
+ * paper lets the exploration step grow; params->eps_halving also halves eps),
  * up to T + 8 steps, after which the search stops (stop_reason 1); a new best
- * state resets both. The collected states are timed in order; after each timing, every
- * transition (s, a, r, s') into it from an already-timed neighbour s joins
- * 𝓜 and one SGD pass over 𝓜 (oldest first) trains the critic (TD(0)) and
- * the actor (δ·∇log π). out->popped counts episodes. params NULL: the defaults. Same ownership and
+ * state resets the walk length and eps. The collected states are timed in
+ * order; after each timing, every transition (s, a, r, s') into it from an
+ * already-timed neighbour s joins 𝓜 (r = 1/cost(s'), §4.1, unless
+ * params->reward selects the log-ratio variant) and one SGD pass over 𝓜
+ * (oldest first) moves every parameter by lr·δ times its gradient — of V(s)
+ * for the critic (TD(0), δ = r + γV(s') − V(s)), of log π(a|s) for the actor —
+ * taken before the update. out->popped counts episodes. params NULL: the defaults. Same ownership and
  * error behaviour as tune_gbfs. */
 int tune_na2c(const gt_space* sp, const gt_tune_opts* opts, const gt_na2c_params* params,
               gt_cost_fn cost, void* ctx, gt_tune_result* out);
+
+/* Releases the device memory the library keeps between calls (the
+ * per-GPU comparison buffers; each GPU's current device is restored).
+ * Must not run concurrently with any other call of the library; later calls
+ * allocate again as needed, so calling it twice, or a GEMM after it, is
+ * fine. GT_EHIP if a hipFree fails (the remaining buffers are still
+ * released). */
+int gt_shutdown(void);
 
 /* Thread-local message of the last failure. */
 const char* gt_last_error(void);

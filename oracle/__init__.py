@@ -8,7 +8,10 @@ built with gcc) through ctypes and shares no code with the GPU library:
   fp64, on the exact widening of the input bytes.
 * ``Space`` — the configuration space of Eq.1–4, rank/unrank in the frozen
   canonical order, legitimacy J (Eq.5), neighbours g(s) (Eq.6, Eq.9).
-* ``gbfs`` — Alg.1 (§4.2) with a caller-supplied cost function.
+* ``gbfs`` — Alg.1 (§4.2) with a caller-supplied cost function;
+  ``random_search`` — the equal-budget baseline (§5); ``na2c`` — Alg.2
+  (§4.3), with ``na2c_probe`` / ``na2c_train`` exposing its networks and
+  its training step.
 
 Parity unpinned: the hardware part of J (register, LDS and grid limits) has
 no value in the paper to pin it; it is checked by hand-worked cases and by
@@ -60,13 +63,21 @@ class _GbfsResult(ctypes.Structure):
 class _Na2cParams(ctypes.Structure):
     _fields_ = [("T", ctypes.c_int32), ("B", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("mem", ctypes.c_int32), ("max_walks", ctypes.c_int32),
+                ("reward", ctypes.c_int32), ("eps_halving", ctypes.c_int32),
                 ("eps", ctypes.c_double), ("gamma", ctypes.c_double), ("lr", ctypes.c_double),
                 ("r_clip", ctypes.c_double)]
 
 
-# N-A2C settings: T = 3 steps per walk (§5), the rest are readings
-NA2C_DEFAULTS = dict(T=3, B=8, H=32, mem=256, max_walks=64, eps=0.8, gamma=0.9, lr=0.01,
-                     r_clip=5.0)
+class _Na2cTransition(ctypes.Structure):
+    _fields_ = [("s", ctypes.c_uint64), ("s2", ctypes.c_uint64), ("a", ctypes.c_int32),
+                ("pad", ctypes.c_int32), ("r", ctypes.c_double)]
+
+
+# N-A2C settings: T = 3 steps per walk (§5) and the reward r = 1/cost(s')
+# of §4.1 (reward=0); the rest are readings. reward=1 (clipped log ratio) and
+# eps_halving=1 are variants.
+NA2C_DEFAULTS = dict(T=3, B=8, H=32, mem=256, max_walks=64, reward=0, eps_halving=0, eps=0.8,
+                     gamma=0.9, lr=0.01, r_clip=5.0)
 
 
 _COST_FN = ctypes.CFUNCTYPE(ctypes.c_double, ctypes.POINTER(_Config), ctypes.c_uint64,
@@ -103,7 +114,8 @@ def lib():
                                        p, p, i64]
         NP = ctypes.POINTER(_Na2cParams)
         L.or_na2c.argtypes = [SP, CF, NP, i64, u64, _COST_FN, p, ctypes.POINTER(_GbfsResult),
-                              p, p, i64]
+                              p, p, i64, p, i64, ctypes.POINTER(i64)]
+        L.or_na2c_train.argtypes = [SP, NP, CF, p, p, CF, i64, p, p]
         L.or_na2c_probe.argtypes = [SP, NP, u64, CF, ctypes.c_int, p, p, p, p, p, p,
                                     ctypes.POINTER(i64), ctypes.POINTER(i64)]
         _lib = L
@@ -331,9 +343,12 @@ def _na2c_params(params=None) -> _Na2cParams:
     return _Na2cParams(**v)
 
 
-def na2c(space: Space, s0, budget: int, seed: int, cost_fn, params=None):
+def na2c(space: Space, s0, budget: int, seed: int, cost_fn, params=None, trace_cap: int = 0):
     """N-A2C (§4.3, Alg.2) with the oracle's readings; ``params`` overrides
-    NA2C_DEFAULTS. Same result dict as gbfs(); ``popped`` counts episodes."""
+    NA2C_DEFAULTS. Same result dict as gbfs(); ``popped`` counts episodes.
+    With trace_cap > 0, ``transitions`` lists the first trace_cap transitions
+    stored into the memory as (rank s, action, r, rank s'), and
+    ``n_transitions`` their total count."""
     log_r = np.zeros(budget, dtype=np.uint64)
     log_c = np.zeros(budget, dtype=np.float64)
 
@@ -343,15 +358,42 @@ def na2c(space: Space, s0, budget: int, seed: int, cost_fn, params=None):
     cb = _COST_FN(_cb)
     res = _GbfsResult()
     prm = _na2c_params(params)
+    tr = (_Na2cTransition * max(1, trace_cap))()
+    n_tr = ctypes.c_int64(0)
     rc = lib().or_na2c(ctypes.byref(space._s), ctypes.byref(space._to_c(s0)), ctypes.byref(prm),
                        int(budget), int(seed), cb, None, ctypes.byref(res), _ptr(log_r),
-                       _ptr(log_c), budget)
+                       _ptr(log_c), budget, ctypes.cast(tr, ctypes.c_void_p) if trace_cap else None,
+                       int(trace_cap), ctypes.byref(n_tr))
     if rc:
         raise ValueError("or_na2c: bad argument")
     n = int(res.timed)
-    return {"best": space._from_c(res.best), "best_cost": float(res.best_cost),
-            "timed": n, "popped": int(res.popped),
-            "log_ranks": [int(v) for v in log_r[:n]], "log_costs": [float(v) for v in log_c[:n]]}
+    out = {"best": space._from_c(res.best), "best_cost": float(res.best_cost),
+           "timed": n, "popped": int(res.popped),
+           "log_ranks": [int(v) for v in log_r[:n]], "log_costs": [float(v) for v in log_c[:n]]}
+    if trace_cap:
+        k = min(trace_cap, n_tr.value)
+        out["transitions"] = [(int(t.s), int(t.a), float(t.r), int(t.s2)) for t in tr[:k]]
+        out["n_transitions"] = n_tr.value
+    return out
+
+
+def na2c_train(space: Space, transitions, actor, critic, params=None):
+    """The oracle's N-A2C training step applied to caller-given flattened
+    parameters (the layout of na2c_probe) for transitions
+    [(s, a, r, s'), …] in order; returns the updated (actor, critic)."""
+    prm = _na2c_params(params)
+    n = len(transitions)
+    S = (_Config * max(1, n))(*[space._to_c(t[0]) for t in transitions])
+    S2 = (_Config * max(1, n))(*[space._to_c(t[3]) for t in transitions])
+    a = np.array([t[1] for t in transitions] or [0], dtype=np.int32)
+    r = np.array([t[2] for t in transitions] or [0.0], dtype=np.float64)
+    th_a = np.array(actor, dtype=np.float64)
+    th_c = np.array(critic, dtype=np.float64)
+    rc = lib().or_na2c_train(ctypes.byref(space._s), ctypes.byref(prm), S, _ptr(a), _ptr(r), S2,
+                             n, _ptr(th_a), _ptr(th_c))
+    if rc:
+        raise ValueError("or_na2c_train: bad argument")
+    return th_a, th_c
 
 
 def na2c_probe(space: Space, cfg, a: int, seed: int = 0, params=None, actor=None, critic=None):

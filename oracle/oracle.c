@@ -350,6 +350,9 @@ int or_legit(const or_space* sp, const or_config* c) {
   if ((BM * BK + BK * BN) * elem > 163840) return 0;
   if (gM * gN * 64 * W > 4294967295LL) return 0; /* work-items per dispatch dimension */
   if (kS > 65535) return 0;
+  /* work-items of the whole dispatch (grid.x · grid.y · threads per group) */
+  const int64_t items = gM * gN * kS * 64 * W;
+  if (items > 4294967295LL) return 0;
   return 1;
 }
 
@@ -577,394 +580,426 @@ int or_random_search(const or_space* sp, int64_t budget, uint64_t seed, or_cost_
   free_tables(&tb);
   return 0;
 }
-
 /* ------------------------------------------------------------------------ */
 /* N-A2C (§4.3, Alg.2).                                                      */
+/*                                                                          */
+/* The two networks are kept as flat parameter vectors,                     */
+/*   actor  θa = [W1 (H×F) | b1 (H) | W2 (A×H) | b2 (A)],                   */
+/*   critic θc = [U1 (H×F) | c1 (H) | u2 (H)   | c2],                       */
+/* each one hidden tanh layer over the state features φ(s); the actor ends  */
+/* in a softmax over the actions available in s, the critic in one linear   */
+/* unit V(s). One training transition (s, a, r, s') takes the TD(0) error   */
+/* δ = r + γ·V(s') − V(s) and the gradients ∇θa log π(a|s) and ∇θc V(s) at  */
+/* the current parameters, then moves both vectors by (lr·δ)·∇.            */
 /* ------------------------------------------------------------------------ */
 
-typedef struct { /* one action of the fixed list: f[x][i] *= 2, f[x][j] /= 2, or the toggle */
-  int x, i, j, toggle;
-} na_action;
+#define NA_MAXF (3 * OR_MAXD + 1)
+#define NA_MAXA (3 * OR_MAXD * (OR_MAXD - 1) + 1)
+#define NA_MAXH 64
 
 typedef struct {
-  int F, A, H;
-  na_action act[3 * OR_MAXD * OR_MAXD + 1];
-  int E[3];
-  int64_t q[3];
-  /* actor */
-  double *W1, *b1, *W2, *b2;
-  /* critic */
-  double *U1, *c1, *u2, c2;
-} na_net;
+  int F, A, H;        /* features, actions, hidden units */
+  int n_actor, n_critic;
+  int mv_x[NA_MAXA];  /* dimension of action a (m, k, n = 0, 1, 2; 3 = MFMA toggle) */
+  int mv_up[NA_MAXA]; /* level whose factor doubles */
+  int mv_dn[NA_MAXA]; /* level whose factor halves */
+  int E[3];           /* power-of-two exponent of each extent */
+  int64_t q[3];       /* odd cofactor of each extent */
+} na_shape;
 
-static void na_actions(const or_space* sp, na_net* n) {
-  n->A = 0;
-  for (int x = 0; x < 3; ++x)
-    for (int i = 0; i < sp->d[x]; ++i)
-      for (int j = 0; j < sp->d[x]; ++j) {
-        if (i == j) continue;
-        if (sp->mode == OR_ADJACENT && abs(i - j) != 1) continue;
-        na_action a = {x, i, j, 0};
-        n->act[n->A++] = a;
-      }
-  if (sp->mfma_coord) {
-    na_action a = {0, 0, 0, 1};
-    n->act[n->A++] = a;
-  }
-}
+/* offsets inside θa and θc */
+#define OFF_W1(z) 0
+#define OFF_B1(z) ((z)->H * (z)->F)
+#define OFF_W2(z) (OFF_B1(z) + (z)->H)
+#define OFF_B2(z) (OFF_W2(z) + (z)->A * (z)->H)
+#define OFF_U1(z) 0
+#define OFF_C1(z) ((z)->H * (z)->F)
+#define OFF_U2(z) (OFF_C1(z) + (z)->H)
+#define OFF_C2(z) (OFF_U2(z) + (z)->H)
 
-static int na_log2(int64_t v) {
+static int exp2_of(int64_t v) {
   int e = 0;
-  while (v > 1) {
-    v >>= 1;
-    ++e;
-  }
+  for (; v > 1; v /= 2) ++e;
   return e;
 }
 
-/* φ(s): exponent share of every level (level 0 without the odd cofactor),
- * then the MFMA bit. */
-static void na_features(const or_space* sp, const na_net* n, const or_config* s, double* phi) {
-  int k = 0;
+/* Action list 𝒜 (Eq.6): per dimension every ordered level pair the mode
+ * allows, then the MFMA toggle when the space has that coordinate. */
+static void na_shape_of(const or_space* sp, int H, na_shape* z) {
+  memset(z, 0, sizeof(*z));
   for (int x = 0; x < 3; ++x)
-    for (int i = 0; i < sp->d[x]; ++i) {
-      const int64_t v = i == 0 ? s->f[x][0] / n->q[x] : s->f[x][i];
-      phi[k++] = n->E[x] ? (double)na_log2(v) / (double)n->E[x] : 0.0;
+    for (int up = 0; up < sp->d[x]; ++up)
+      for (int dn = 0; dn < sp->d[x]; ++dn) {
+        const int adjacent = up - dn == 1 || dn - up == 1;
+        if (up == dn || (sp->mode == OR_ADJACENT && !adjacent)) continue;
+        z->mv_x[z->A] = x;
+        z->mv_up[z->A] = up;
+        z->mv_dn[z->A] = dn;
+        z->A++;
+      }
+  if (sp->mfma_coord) {
+    z->mv_x[z->A] = 3;
+    z->A++;
+  }
+  z->F = sp->d[0] + sp->d[1] + sp->d[2] + (sp->mfma_coord ? 1 : 0);
+  z->H = H;
+  z->n_actor = H * z->F + H + z->A * H + z->A;
+  z->n_critic = H * z->F + H + H + 1;
+  const int64_t ext[3] = {sp->M, sp->K, sp->N};
+  for (int x = 0; x < 3; ++x) {
+    z->q[x] = odd_part(ext[x]);
+    z->E[x] = exp2_of(ext[x] / z->q[x]);
+  }
+}
+
+/* φ(s): each level's exponent as a share of its dimension's E (level 0
+ * without the odd cofactor), then 1 for MFMA 32. */
+static void na_phi(const or_space* sp, const na_shape* z, const or_config* s, double* phi) {
+  int f = 0;
+  for (int x = 0; x < 3; ++x)
+    for (int lvl = 0; lvl < sp->d[x]; ++lvl) {
+      const int64_t v = lvl == 0 ? s->f[x][0] / z->q[x] : s->f[x][lvl];
+      phi[f++] = z->E[x] == 0 ? 0.0 : (double)exp2_of(v) / (double)z->E[x];
     }
-  if (sp->mfma_coord) phi[k++] = s->mfma == 32 ? 1.0 : 0.0;
+  if (sp->mfma_coord) phi[f++] = s->mfma == 32 ? 1.0 : 0.0;
 }
 
-static int na_available(const na_net* n, const or_config* s, int a) {
-  const na_action* ac = &n->act[a];
-  if (ac->toggle) return 1;
-  return s->f[ac->x][ac->j] % 2 == 0;
+/* a is available in s when the halved factor is even (the result stays a
+ * positive integer, Eq.6); the toggle always is. */
+static int na_ok(const na_shape* z, const or_config* s, int a) {
+  if (z->mv_x[a] == 3) return 1;
+  return s->f[z->mv_x[a]][z->mv_dn[a]] % 2 == 0;
 }
 
-static or_config na_step(const na_net* n, const or_config* s, int a) {
+static void na_ok_all(const na_shape* z, const or_config* s, int* ok) {
+  for (int a = 0; a < z->A; ++a) ok[a] = na_ok(z, s, a);
+}
+
+/* s' = step(s, a), Eq.7 */
+static or_config na_move(const na_shape* z, const or_config* s, int a) {
   or_config t = *s;
-  const na_action* ac = &n->act[a];
-  if (ac->toggle) {
+  if (z->mv_x[a] == 3) {
     t.mfma = s->mfma == 16 ? 32 : 16;
   } else {
-    t.f[ac->x][ac->i] = s->f[ac->x][ac->i] * 2;
-    t.f[ac->x][ac->j] = s->f[ac->x][ac->j] / 2;
+    t.f[z->mv_x[a]][z->mv_up[a]] *= 2;
+    t.f[z->mv_x[a]][z->mv_dn[a]] /= 2;
   }
   return t;
 }
 
-/* the action that undoes a (from step(s, a) back to s) */
-static int na_inverse(const na_net* n, int a) {
-  const na_action* ac = &n->act[a];
-  if (ac->toggle) return a;
-  for (int b = 0; b < n->A; ++b)
-    if (!n->act[b].toggle && n->act[b].x == ac->x && n->act[b].i == ac->j && n->act[b].j == ac->i)
+/* the action leading back: same dimension, the two levels swapped */
+static int na_back(const na_shape* z, int a) {
+  if (z->mv_x[a] == 3) return a;
+  for (int b = 0; b < z->A; ++b)
+    if (z->mv_x[b] == z->mv_x[a] && z->mv_up[b] == z->mv_dn[a] && z->mv_dn[b] == z->mv_up[a])
       return b;
   return -1;
 }
 
-static double na_uniform(uint64_t* st) {
-  return (double)(or_splitmix64_next(st) >> 11) * (1.0 / 9007199254740992.0);
-}
-
-static int na_alloc(const or_space* sp, const or_na2c_params* prm, uint64_t seed, na_net* n) {
-  memset(n, 0, sizeof(*n));
-  na_actions(sp, n);
-  n->F = sp->d[0] + sp->d[1] + sp->d[2] + (sp->mfma_coord ? 1 : 0);
-  n->H = prm->H;
-  const int64_t ext[3] = {sp->M, sp->K, sp->N};
-  for (int x = 0; x < 3; ++x) {
-    n->q[x] = odd_part(ext[x]);
-    n->E[x] = na_log2(ext[x] / n->q[x]);
+/* y[o] = tanh(b[o] + Σ_i W[o][i]·x[i]) */
+static void tanh_layer(const double* W, const double* b, int n_out, int n_in, const double* x,
+                       double* y) {
+  for (int o = 0; o < n_out; ++o) {
+    double acc = b[o];
+    for (int i = 0; i < n_in; ++i) acc += W[o * n_in + i] * x[i];
+    y[o] = tanh(acc);
   }
-  const int F = n->F, A = n->A, H = n->H;
-  n->W1 = (double*)calloc((size_t)(H * F), sizeof(double));
-  n->b1 = (double*)calloc((size_t)H, sizeof(double));
-  n->W2 = (double*)calloc((size_t)(A * H), sizeof(double));
-  n->b2 = (double*)calloc((size_t)A, sizeof(double));
-  n->U1 = (double*)calloc((size_t)(H * F), sizeof(double));
-  n->c1 = (double*)calloc((size_t)H, sizeof(double));
-  n->u2 = (double*)calloc((size_t)H, sizeof(double));
-  if (!n->W1 || !n->b1 || !n->W2 || !n->b2 || !n->U1 || !n->c1 || !n->u2) return -1;
-  /* weights U(−1/√fan_in, 1/√fan_in) in the order W1, W2, U1, u2; biases 0 */
-  uint64_t ws = seed ^ 0xA2C0A2C0A2C0A2C0ULL;
-  const double bF = 1.0 / sqrt((double)F), bH = 1.0 / sqrt((double)H);
-  for (int k = 0; k < H * F; ++k) n->W1[k] = (2.0 * na_uniform(&ws) - 1.0) * bF;
-  for (int k = 0; k < A * H; ++k) n->W2[k] = (2.0 * na_uniform(&ws) - 1.0) * bH;
-  for (int k = 0; k < H * F; ++k) n->U1[k] = (2.0 * na_uniform(&ws) - 1.0) * bF;
-  for (int k = 0; k < H; ++k) n->u2[k] = (2.0 * na_uniform(&ws) - 1.0) * bH;
-  n->c2 = 0.0;
-  return 0;
 }
 
-static void na_free(na_net* n) {
-  free(n->W1);
-  free(n->b1);
-  free(n->W2);
-  free(n->b2);
-  free(n->U1);
-  free(n->c1);
-  free(n->u2);
-}
-
-/* actor forward: hidden h[H], π over the available actions (0 elsewhere) */
-static void na_actor(const na_net* n, const double* phi, const int* avail, double* h,
-                     double* pi) {
-  for (int k = 0; k < n->H; ++k) {
-    double z = n->b1[k];
-    for (int f = 0; f < n->F; ++f) z += n->W1[k * n->F + f] * phi[f];
-    h[k] = tanh(z);
+/* π(·|s) with hidden activations h; π = 0 on unavailable actions */
+static void actor_pi(const na_shape* z, const double* th, const double* phi, const int* ok,
+                     double* h, double* pi) {
+  tanh_layer(th + OFF_W1(z), th + OFF_B1(z), z->H, z->F, phi, h);
+  const double* W2 = th + OFF_W2(z);
+  const double* b2 = th + OFF_B2(z);
+  double top = -INFINITY;
+  for (int a = 0; a < z->A; ++a) {
+    pi[a] = 0.0;
+    if (!ok[a]) continue;
+    double logit = b2[a];
+    for (int k = 0; k < z->H; ++k) logit += W2[a * z->H + k] * h[k];
+    pi[a] = logit;
+    if (logit > top) top = logit;
   }
-  double zmax = -INFINITY;
-  for (int a = 0; a < n->A; ++a) {
-    if (!avail[a]) {
-      pi[a] = 0.0;
-      continue;
+  double norm = 0.0;
+  for (int a = 0; a < z->A; ++a)
+    if (ok[a]) {
+      pi[a] = exp(pi[a] - top);
+      norm += pi[a];
     }
-    double z = n->b2[a];
-    for (int k = 0; k < n->H; ++k) z += n->W2[a * n->H + k] * h[k];
-    pi[a] = z;
-    if (z > zmax) zmax = z;
-  }
-  double sum = 0.0;
-  for (int a = 0; a < n->A; ++a)
-    if (avail[a]) {
-      pi[a] = exp(pi[a] - zmax);
-      sum += pi[a];
-    }
-  for (int a = 0; a < n->A; ++a)
-    if (avail[a]) pi[a] /= sum;
+  for (int a = 0; a < z->A; ++a)
+    if (ok[a]) pi[a] /= norm;
 }
 
-static double na_critic(const na_net* n, const double* phi, double* g) {
-  double v = n->c2;
-  for (int k = 0; k < n->H; ++k) {
-    double z = n->c1[k];
-    for (int f = 0; f < n->F; ++f) z += n->U1[k * n->F + f] * phi[f];
-    g[k] = tanh(z);
-    v += n->u2[k] * g[k];
-  }
+/* V(s) with hidden activations g */
+static double critic_v(const na_shape* z, const double* th, const double* phi, double* g) {
+  tanh_layer(th + OFF_U1(z), th + OFF_C1(z), z->H, z->F, phi, g);
+  const double* u2 = th + OFF_U2(z);
+  double v = th[OFF_C2(z)];
+  for (int k = 0; k < z->H; ++k) v += u2[k] * g[k];
   return v;
 }
 
-typedef struct {
-  double phi[3 * OR_MAXD + 1], phi2[3 * OR_MAXD + 1];
-  int avail[3 * OR_MAXD * OR_MAXD + 1];
+/* ∇θa log π(a|s). With e_b = [b = a] − π_b over the available b:
+ * ∂/∂b2_b = e_b, ∂/∂W2_bk = e_b·h_k, ∂/∂b1_k = (Σ_b e_b·W2_bk)(1 − h_k²),
+ * ∂/∂W1_kf = ∂/∂b1_k · φ_f. */
+static void actor_grad(const na_shape* z, const double* th, const double* phi, const int* ok,
+                       int a, double* grad) {
+  double h[NA_MAXH], pi[NA_MAXA], e[NA_MAXA];
+  actor_pi(z, th, phi, ok, h, pi);
+  for (int b = 0; b < z->A; ++b) e[b] = ok[b] ? (b == a ? 1.0 : 0.0) - pi[b] : 0.0;
+  const double* W2 = th + OFF_W2(z);
+  for (int k = 0; k < z->H; ++k) {
+    double back = 0.0;
+    for (int b = 0; b < z->A; ++b)
+      if (ok[b]) back += e[b] * W2[b * z->H + k];
+    const double dz = back * (1.0 - h[k] * h[k]);
+    for (int f = 0; f < z->F; ++f) grad[OFF_W1(z) + k * z->F + f] = dz * phi[f];
+    grad[OFF_B1(z) + k] = dz;
+  }
+  for (int b = 0; b < z->A; ++b) {
+    for (int k = 0; k < z->H; ++k) grad[OFF_W2(z) + b * z->H + k] = e[b] * h[k];
+    grad[OFF_B2(z) + b] = e[b];
+  }
+}
+
+/* ∇θc V(s): ∂/∂c2 = 1, ∂/∂u2_k = g_k, ∂/∂c1_k = u2_k(1 − g_k²),
+ * ∂/∂U1_kf = ∂/∂c1_k · φ_f. */
+static void critic_grad(const na_shape* z, const double* th, const double* phi, double* grad) {
+  double g[NA_MAXH];
+  critic_v(z, th, phi, g);
+  const double* u2 = th + OFF_U2(z);
+  for (int k = 0; k < z->H; ++k) {
+    const double dz = u2[k] * (1.0 - g[k] * g[k]);
+    for (int f = 0; f < z->F; ++f) grad[OFF_U1(z) + k * z->F + f] = dz * phi[f];
+    grad[OFF_C1(z) + k] = dz;
+    grad[OFF_U2(z) + k] = g[k];
+  }
+  grad[OFF_C2(z)] = 1.0;
+}
+
+typedef struct { /* a transition (s, a, r, s') as the networks see it */
+  double phi[NA_MAXF], phi2[NA_MAXF];
+  int ok[NA_MAXA];
   int a;
   double r;
-} na_trans;
+} na_sample;
 
-/* one transition: δ from the current critic, then the critic's and the
- * actor's updates (both with gradients at the pre-update weights) */
-static void na_train_one(na_net* n, const na_trans* t, double gamma, double lr, double* h,
-                         double* g, double* pi, double* dh) {
-  double g2[64];
-  const double v2 = na_critic(n, t->phi2, g2);
-  const double v = na_critic(n, t->phi, g);
-  const double delta = t->r + gamma * v2 - v;
-  /* critic: θ += lr·δ·∂V(s)/∂θ */
-  for (int k = 0; k < n->H; ++k) {
-    const double back = n->u2[k] * (1.0 - g[k] * g[k]);
-    for (int f = 0; f < n->F; ++f) n->U1[k * n->F + f] += lr * delta * back * t->phi[f];
-    n->c1[k] += lr * delta * back;
-  }
-  for (int k = 0; k < n->H; ++k) n->u2[k] += lr * delta * g[k];
-  n->c2 += lr * delta;
-  /* actor: θ += lr·δ·∇ log π(a|s) */
-  na_actor(n, t->phi, t->avail, h, pi);
-  for (int k = 0; k < n->H; ++k) {
-    double s = 0.0;
-    for (int b = 0; b < n->A; ++b) {
-      if (!t->avail[b]) continue;
-      const double e = (b == t->a ? 1.0 : 0.0) - pi[b];
-      s += e * n->W2[b * n->H + k];
-    }
-    dh[k] = s * (1.0 - h[k] * h[k]);
-  }
-  for (int b = 0; b < n->A; ++b) {
-    if (!t->avail[b]) continue;
-    const double e = (b == t->a ? 1.0 : 0.0) - pi[b];
-    for (int k = 0; k < n->H; ++k) n->W2[b * n->H + k] += lr * delta * e * h[k];
-    n->b2[b] += lr * delta * e;
-  }
-  for (int k = 0; k < n->H; ++k) {
-    for (int f = 0; f < n->F; ++f) n->W1[k * n->F + f] += lr * delta * dh[k] * t->phi[f];
-    n->b1[k] += lr * delta * dh[k];
-  }
+/* One advantage actor-critic update on one transition. */
+static void td_update(const na_shape* z, double* tha, double* thc, const na_sample* t,
+                      double gamma, double lr) {
+  double g[NA_MAXH], ga[NA_MAXH * NA_MAXF + NA_MAXH + NA_MAXA * NA_MAXH + NA_MAXA];
+  double gc[NA_MAXH * NA_MAXF + 2 * NA_MAXH + 1];
+  const double v_next = critic_v(z, thc, t->phi2, g);
+  const double v_now = critic_v(z, thc, t->phi, g);
+  const double delta = t->r + gamma * v_next - v_now;
+  actor_grad(z, tha, t->phi, t->ok, t->a, ga);
+  critic_grad(z, thc, t->phi, gc);
+  const double step = lr * delta;
+  for (int k = 0; k < z->n_critic; ++k) thc[k] += step * gc[k];
+  for (int k = 0; k < z->n_actor; ++k) tha[k] += step * ga[k];
 }
 
-/* visited hashtable H_v: rank → cost (open addressing) */
+/* Initial parameters: U(−1/√fan_in, 1/√fan_in) from SplitMix64(seed ^
+ * 0xA2C0A2C0A2C0A2C0), drawn in the order W1, W2, U1, u2; biases 0. */
+static double unit_draw(uint64_t* st) {
+  return (double)(or_splitmix64_next(st) >> 11) * (1.0 / 9007199254740992.0);
+}
+
+static void na_init_params(const na_shape* z, uint64_t seed, double* tha, double* thc) {
+  memset(tha, 0, sizeof(double) * (size_t)z->n_actor);
+  memset(thc, 0, sizeof(double) * (size_t)z->n_critic);
+  uint64_t st = seed ^ 0xA2C0A2C0A2C0A2C0ULL;
+  const double lim_f = 1.0 / sqrt((double)z->F), lim_h = 1.0 / sqrt((double)z->H);
+  for (int k = 0; k < z->H * z->F; ++k) tha[OFF_W1(z) + k] = (2.0 * unit_draw(&st) - 1.0) * lim_f;
+  for (int k = 0; k < z->A * z->H; ++k) tha[OFF_W2(z) + k] = (2.0 * unit_draw(&st) - 1.0) * lim_h;
+  for (int k = 0; k < z->H * z->F; ++k) thc[OFF_U1(z) + k] = (2.0 * unit_draw(&st) - 1.0) * lim_f;
+  for (int k = 0; k < z->H; ++k) thc[OFF_U2(z) + k] = (2.0 * unit_draw(&st) - 1.0) * lim_h;
+}
+
+/* r(s, a) of a transition into s'. Default (§4.1): 1/cost(s'), so a failed
+ * s' (cost +∞) earns 0. Variant: log(cost(s)/cost(s')) clipped to ±clip. */
+static double na_r(int mode, double cost_s, double cost_s2, double clip) {
+  if (mode == 0) return 1.0 / cost_s2;
+  if (isinf(cost_s2)) return isinf(cost_s) ? 0.0 : -clip;
+  if (isinf(cost_s)) return clip;
+  const double r = log(cost_s / cost_s2);
+  return r > clip ? clip : (r < -clip ? -clip : r);
+}
+
+/* H_v: rank → cost, open addressing */
 typedef struct {
   uint64_t* key;
-  double* val;
-  unsigned char* used;
+  double* cost;
+  unsigned char* full;
   uint64_t cap;
-} na_map;
+} na_table;
 
-static uint64_t na_slot(const na_map* m, uint64_t r) {
-  uint64_t h = (r * 0x9E3779B97F4A7C15ULL) % m->cap;
-  while (m->used[h] && m->key[h] != r) h = (h + 1) % m->cap;
-  return h;
+static uint64_t na_find(const na_table* t, uint64_t r) {
+  uint64_t i = (r * 0x9E3779B97F4A7C15ULL) % t->cap;
+  while (t->full[i] && t->key[i] != r) i = (i + 1) % t->cap;
+  return i;
 }
 
-static double na_reward(double cs, double cs2, double clip) {
-  if (isinf(cs2)) return isinf(cs) ? 0.0 : -clip;
-  if (isinf(cs)) return clip;
-  double r = log(cs / cs2);
-  if (r > clip) r = clip;
-  if (r < -clip) r = -clip;
-  return r;
+static int params_bad(const or_na2c_params* p) {
+  return p->T < 1 || p->B < 1 || p->H < 1 || p->H > NA_MAXH || p->mem < 1 || p->max_walks < 1 ||
+         (p->reward != 0 && p->reward != 1) || (p->eps_halving != 0 && p->eps_halving != 1);
+}
+
+/* a ∈ 𝒜 drawn for one walk step in s: with probability ε from π(·|s)
+ * (inverse CDF over the available actions in list order), else uniformly
+ * among the available ones */
+static int na_pick(const or_space* sp, const na_shape* z, const double* tha, const or_config* s,
+                   double eps, uint64_t* rng) {
+  int ok[NA_MAXA];
+  na_ok_all(z, s, ok);
+  int n_ok = 0;
+  for (int b = 0; b < z->A; ++b) n_ok += ok[b];
+  if (unit_draw(rng) < eps) {
+    double phi[NA_MAXF], h[NA_MAXH], pi[NA_MAXA];
+    na_phi(sp, z, s, phi);
+    actor_pi(z, tha, phi, ok, h, pi);
+    const double u = unit_draw(rng);
+    int pick = -1;
+    double cdf = 0.0;
+    for (int b = 0; b < z->A; ++b) {
+      if (!ok[b]) continue;
+      pick = b; /* the last available action if rounding leaves u ≥ Σπ */
+      cdf += pi[b];
+      if (u < cdf) break;
+    }
+    return pick;
+  }
+  uint64_t k = or_splitmix64_next(rng) % (uint64_t)n_ok;
+  for (int b = 0; b < z->A; ++b)
+    if (ok[b] && k-- == 0) return b;
+  return -1;
 }
 
 int or_na2c(const or_space* sp, const or_config* s0, const or_na2c_params* prm,
             int64_t budget, uint64_t seed, or_cost_fn cost, void* ctx, or_gbfs_result* res,
-            uint64_t* log_ranks, double* log_costs, int64_t log_cap) {
+            uint64_t* log_ranks, double* log_costs, int64_t log_cap,
+            or_na2c_transition* trace, int64_t trace_cap, int64_t* trace_n) {
   uint64_t size;
   if (or_space_size(sp, &size) || !s0 || !prm || !cost || !res) return -1;
-  if (budget < 1 || prm->T < 1 || prm->B < 1 || prm->H < 1 || prm->H > 64 || prm->mem < 1 ||
-      prm->max_walks < 1 || !or_legit(sp, s0))
-    return -1;
+  if (budget < 1 || params_bad(prm) || !or_legit(sp, s0)) return -1;
   tables tb;
   build_tables(sp, &tb);
-  na_net n;
-  if (na_alloc(sp, prm, seed, &n)) return -1;
-  na_map hv;
+  na_shape z;
+  na_shape_of(sp, prm->H, &z);
+  double* tha = (double*)malloc(sizeof(double) * (size_t)z.n_actor);
+  double* thc = (double*)malloc(sizeof(double) * (size_t)z.n_critic);
+  na_table hv;
   hv.cap = (uint64_t)budget * 4 + 17;
   hv.key = (uint64_t*)calloc(hv.cap, sizeof(uint64_t));
-  hv.val = (double*)calloc(hv.cap, sizeof(double));
-  hv.used = (unsigned char*)calloc(hv.cap, 1);
-  na_trans* mem = (na_trans*)calloc((size_t)prm->mem, sizeof(na_trans));
-  or_config* coll = (or_config*)calloc((size_t)prm->B, sizeof(or_config));
-  uint64_t* coll_r = (uint64_t*)calloc((size_t)prm->B, sizeof(uint64_t));
-  double h[64], g[64], dh[64], pi[3 * OR_MAXD * OR_MAXD + 1];
-  int64_t mem_n = 0, mem_head = 0; /* FIFO: oldest at mem_head */
+  hv.cost = (double*)calloc(hv.cap, sizeof(double));
+  hv.full = (unsigned char*)calloc(hv.cap, 1);
+  na_sample* M = (na_sample*)calloc((size_t)prm->mem, sizeof(na_sample));
+  or_config* batch = (or_config*)calloc((size_t)prm->B, sizeof(or_config));
+  uint64_t* batch_r = (uint64_t*)calloc((size_t)prm->B, sizeof(uint64_t));
+  if (!tha || !thc || !hv.key || !hv.cost || !hv.full || !M || !batch || !batch_r) {
+    free(tha), free(thc), free(hv.key), free(hv.cost), free(hv.full), free(M), free(batch),
+        free(batch_r);
+    free_tables(&tb);
+    return -1;
+  }
+  na_init_params(&z, seed, tha, thc);
+  int64_t m_len = 0, m_old = 0; /* FIFO 𝓜: m_len entries from m_old */
+  int64_t n_trace = 0;
   uint64_t rng = seed;
   int64_t timed = 0, episodes = 0;
 
+  /* s0 is timed first and is the first centre */
   uint64_t r0;
   rank_with(sp, &tb, s0, &r0);
-  or_config c0cfg = *s0;
-  const double c0 = cost(&c0cfg, r0, ctx);
-  if (timed < log_cap) {
-    log_ranks[timed] = r0;
-    log_costs[timed] = c0;
-  }
+  or_config first = *s0;
+  const double c0 = cost(&first, r0, ctx);
+  if (timed < log_cap) log_ranks[timed] = r0, log_costs[timed] = c0;
   ++timed;
-  {
-    const uint64_t sl = na_slot(&hv, r0);
-    hv.used[sl] = 1;
-    hv.key[sl] = r0;
-    hv.val[sl] = c0;
-  }
+  uint64_t slot = na_find(&hv, r0);
+  hv.full[slot] = 1, hv.key[slot] = r0, hv.cost[slot] = c0;
   double cost_min = c0;
   uint64_t best = r0;
-  or_config center = *s0;
+  or_config centre = *s0;
 
-  int steps = prm->T;      /* walk length; grows while episodes collect nothing */
-  double eps_cur = prm->eps; /* share of policy steps; halves with each such episode */
+  int walk = prm->T;    /* 𝒯: grows by one after an episode that collects nothing */
+  double eps = prm->eps; /* halves with such an episode when eps_halving is set */
   while (timed < budget) {
-    /* collect B unvisited legitimate states by walks of `steps` steps from
-     * the centre */
+    /* B_collect: walks of `walk` steps from the centre until B states that
+     * are legitimate, not in H_v and not yet collected are found */
     int nb = 0;
     for (int w = 0; w < prm->max_walks && nb < prm->B; ++w) {
-      or_config s = center;
-      for (int t = 0; t < steps; ++t) {
-        double phi[3 * OR_MAXD + 1];
-        int avail[3 * OR_MAXD * OR_MAXD + 1], navail = 0;
-        for (int a = 0; a < n.A; ++a) {
-          avail[a] = na_available(&n, &s, a);
-          navail += avail[a];
-        }
-        int a = -1;
-        if (na_uniform(&rng) < eps_cur) {
-          na_features(sp, &n, &s, phi);
-          na_actor(&n, phi, avail, h, pi);
-          const double u = na_uniform(&rng);
-          double cum = 0.0;
-          for (int b = 0; b < n.A; ++b) {
-            if (!avail[b]) continue;
-            a = b; /* the last available action if rounding leaves u ≥ Σπ */
-            cum += pi[b];
-            if (u < cum) break;
-          }
-        } else {
-          int k = (int)(or_splitmix64_next(&rng) % (uint64_t)navail);
-          for (int b = 0; b < n.A; ++b)
-            if (avail[b] && k-- == 0) {
-              a = b;
-              break;
-            }
-        }
-        const or_config s2 = na_step(&n, &s, a);
-        if (or_legit(sp, &s2)) {
+      or_config s = centre;
+      for (int t = 0; t < walk; ++t) {
+        const int a = na_pick(sp, &z, tha, &s, eps, &rng);
+        const or_config s2 = na_move(&z, &s, a);
+        if (or_legit(sp, &s2) && nb < prm->B) {
           uint64_t r2;
           rank_with(sp, &tb, &s2, &r2);
-          int dup = hv.used[na_slot(&hv, r2)];
-          for (int b = 0; b < nb && !dup; ++b) dup = coll_r[b] == r2;
-          if (!dup && nb < prm->B) {
-            coll[nb] = s2;
-            coll_r[nb] = r2;
-            ++nb;
-          }
+          int seen = hv.full[na_find(&hv, r2)];
+          for (int b = 0; b < nb; ++b) seen = seen || batch_r[b] == r2;
+          if (!seen) batch[nb] = s2, batch_r[nb] = r2, ++nb;
         }
         s = s2;
       }
     }
     ++episodes;
     if (nb == 0) {
-      /* nothing new within `steps` of the centre: walk one step further
-       * (§4.3 lets the exploration step grow) and halve the share of policy
-       * steps, up to T + 8 */
-      if (steps >= prm->T + 8) break;
-      ++steps;
-      eps_cur *= 0.5;
+      if (walk >= prm->T + 8) break;
+      ++walk;
+      if (prm->eps_halving) eps *= 0.5;
       continue;
     }
     for (int b = 0; b < nb && timed < budget; ++b) {
-      or_config sc = coll[b];
-      const double c = cost(&sc, coll_r[b], ctx);
-      if (timed < log_cap) {
-        log_ranks[timed] = coll_r[b];
-        log_costs[timed] = c;
-      }
+      or_config sb = batch[b];
+      const double c = cost(&sb, batch_r[b], ctx);
+      if (timed < log_cap) log_ranks[timed] = batch_r[b], log_costs[timed] = c;
       ++timed;
-      if (c < cost_min) {
+      if (c < cost_min) { /* new s*: the next episode walks from it */
         cost_min = c;
-        best = coll_r[b];
-        center = coll[b];
-        steps = prm->T; /* a new centre: back to T-step walks and ε */
-        eps_cur = prm->eps;
+        best = batch_r[b];
+        centre = batch[b];
+        walk = prm->T;
+        eps = prm->eps;
       }
-      const uint64_t sl = na_slot(&hv, coll_r[b]);
-      hv.used[sl] = 1;
-      hv.key[sl] = coll_r[b];
-      hv.val[sl] = c;
-      /* every (s, a) with step(s, a) = s' and s already timed */
-      for (int bb = 0; bb < n.A; ++bb) {
-        if (!na_available(&n, &coll[b], bb)) continue;
-        const or_config p = na_step(&n, &coll[b], bb);
-        if (!or_member(sp, &p)) continue;
-        uint64_t rp;
-        rank_with(sp, &tb, &p, &rp);
-        const uint64_t ps = na_slot(&hv, rp);
-        if (!hv.used[ps]) continue;
-        na_trans tr;
-        memset(&tr, 0, sizeof(tr));
-        na_features(sp, &n, &p, tr.phi);
-        na_features(sp, &n, &coll[b], tr.phi2);
-        for (int a = 0; a < n.A; ++a) tr.avail[a] = na_available(&n, &p, a);
-        tr.a = na_inverse(&n, bb);
-        tr.r = na_reward(hv.val[ps], c, prm->r_clip);
-        if (mem_n < prm->mem) {
-          mem[(mem_head + mem_n) % prm->mem] = tr;
-          ++mem_n;
-        } else {
-          mem[mem_head] = tr;
-          mem_head = (mem_head + 1) % prm->mem;
+      slot = na_find(&hv, batch_r[b]);
+      hv.full[slot] = 1, hv.key[slot] = batch_r[b], hv.cost[slot] = c;
+      /* 𝓜 gains (s, a, r, s') for every timed s with step(s, a) = s':
+       * s = step(s', a') over the available a', and a leads back */
+      for (int ap = 0; ap < z.A; ++ap) {
+        if (!na_ok(&z, &batch[b], ap)) continue;
+        const or_config s = na_move(&z, &batch[b], ap);
+        if (!or_member(sp, &s)) continue;
+        uint64_t rs;
+        rank_with(sp, &tb, &s, &rs);
+        const uint64_t ps = na_find(&hv, rs);
+        if (!hv.full[ps]) continue;
+        na_sample smp;
+        memset(&smp, 0, sizeof(smp));
+        na_phi(sp, &z, &s, smp.phi);
+        na_phi(sp, &z, &batch[b], smp.phi2);
+        na_ok_all(&z, &s, smp.ok);
+        smp.a = na_back(&z, ap);
+        smp.r = na_r(prm->reward, hv.cost[ps], c, prm->r_clip);
+        if (trace && n_trace < trace_cap) {
+          trace[n_trace].s = rs;
+          trace[n_trace].s2 = batch_r[b];
+          trace[n_trace].a = smp.a;
+          trace[n_trace].pad = 0;
+          trace[n_trace].r = smp.r;
+        }
+        ++n_trace;
+        if (m_len < prm->mem) {
+          M[(m_old + m_len) % prm->mem] = smp;
+          ++m_len;
+        } else { /* full: the oldest entry is replaced */
+          M[m_old] = smp;
+          m_old = (m_old + 1) % prm->mem;
         }
       }
-      /* one pass over M, oldest first */
-      for (int64_t k = 0; k < mem_n; ++k)
-        na_train_one(&n, &mem[(mem_head + k) % prm->mem], prm->gamma, prm->lr, h, g, pi, dh);
+      /* train on 𝓜, oldest transition first */
+      for (int64_t k = 0; k < m_len; ++k)
+        td_update(&z, tha, thc, &M[(m_old + k) % prm->mem], prm->gamma, prm->lr);
     }
   }
   unrank_with(sp, &tb, best, &res->best);
@@ -972,13 +1007,9 @@ int or_na2c(const or_space* sp, const or_config* s0, const or_na2c_params* prm,
   res->best_cost = cost_min;
   res->timed = timed;
   res->popped = episodes;
-  free(hv.key);
-  free(hv.val);
-  free(hv.used);
-  free(mem);
-  free(coll);
-  free(coll_r);
-  na_free(&n);
+  if (trace_n) *trace_n = n_trace;
+  free(tha), free(thc), free(hv.key), free(hv.cost), free(hv.full), free(M), free(batch),
+      free(batch_r);
   free_tables(&tb);
   return 0;
 }
@@ -988,61 +1019,52 @@ int or_na2c_probe(const or_space* sp, const or_na2c_params* prm, uint64_t seed,
                   const double* critic_params, double* pi, double* v,
                   double* g_actor, double* g_critic, int64_t* n_actor, int64_t* n_critic) {
   uint64_t size;
-  if (or_space_size(sp, &size) || !prm || prm->H < 1 || prm->H > 64) return -1;
-  na_net n;
-  if (na_alloc(sp, prm, seed, &n)) return -1;
-  const int F = n.F, A = n.A, H = n.H;
-  const int64_t na = (int64_t)H * F + H + (int64_t)A * H + A, nc = (int64_t)H * F + H + H + 1;
-  if (n_actor) *n_actor = na;
-  if (n_critic) *n_critic = nc;
-  if (!s || !pi || !v || !g_actor || !g_critic || a < 0 || a >= A) {
-    na_free(&n);
-    return 0;
+  if (or_space_size(sp, &size) || !prm || prm->H < 1 || prm->H > NA_MAXH) return -1;
+  na_shape z;
+  na_shape_of(sp, prm->H, &z);
+  if (n_actor) *n_actor = z.n_actor;
+  if (n_critic) *n_critic = z.n_critic;
+  if (!s || !pi || !v || !g_actor || !g_critic || a < 0 || a >= z.A) return 0;
+  double* tha = (double*)malloc(sizeof(double) * (size_t)z.n_actor);
+  double* thc = (double*)malloc(sizeof(double) * (size_t)z.n_critic);
+  if (!tha || !thc) {
+    free(tha), free(thc);
+    return -1;
   }
-  if (actor_params) {
-    int64_t k = 0;
-    for (int t = 0; t < H * F; ++t) n.W1[t] = actor_params[k++];
-    for (int t = 0; t < H; ++t) n.b1[t] = actor_params[k++];
-    for (int t = 0; t < A * H; ++t) n.W2[t] = actor_params[k++];
-    for (int t = 0; t < A; ++t) n.b2[t] = actor_params[k++];
+  na_init_params(&z, seed, tha, thc);
+  if (actor_params) memcpy(tha, actor_params, sizeof(double) * (size_t)z.n_actor);
+  if (critic_params) memcpy(thc, critic_params, sizeof(double) * (size_t)z.n_critic);
+  double phi[NA_MAXF], h[NA_MAXH], g[NA_MAXH];
+  int ok[NA_MAXA];
+  na_phi(sp, &z, s, phi);
+  na_ok_all(&z, s, ok);
+  actor_pi(&z, tha, phi, ok, h, pi);
+  *v = critic_v(&z, thc, phi, g);
+  actor_grad(&z, tha, phi, ok, a, g_actor);
+  critic_grad(&z, thc, phi, g_critic);
+  free(tha), free(thc);
+  return 0;
+}
+
+int or_na2c_train(const or_space* sp, const or_na2c_params* prm, const or_config* s,
+                  const int* a, const double* r, const or_config* s2, int64_t n,
+                  double* actor_params, double* critic_params) {
+  uint64_t size;
+  if (or_space_size(sp, &size) || !prm || prm->H < 1 || prm->H > NA_MAXH || n < 0 ||
+      (n > 0 && (!s || !a || !r || !s2)) || !actor_params || !critic_params)
+    return -1;
+  na_shape z;
+  na_shape_of(sp, prm->H, &z);
+  for (int64_t t = 0; t < n; ++t) {
+    na_sample smp;
+    memset(&smp, 0, sizeof(smp));
+    if (a[t] < 0 || a[t] >= z.A || !na_ok(&z, &s[t], a[t])) return -1;
+    na_phi(sp, &z, &s[t], smp.phi);
+    na_phi(sp, &z, &s2[t], smp.phi2);
+    na_ok_all(&z, &s[t], smp.ok);
+    smp.a = a[t];
+    smp.r = r[t];
+    td_update(&z, actor_params, critic_params, &smp, prm->gamma, prm->lr);
   }
-  if (critic_params) {
-    int64_t k = 0;
-    for (int t = 0; t < H * F; ++t) n.U1[t] = critic_params[k++];
-    for (int t = 0; t < H; ++t) n.c1[t] = critic_params[k++];
-    for (int t = 0; t < H; ++t) n.u2[t] = critic_params[k++];
-    n.c2 = critic_params[k++];
-  }
-  double phi[3 * OR_MAXD + 1], h[64], g[64];
-  int avail[3 * OR_MAXD * OR_MAXD + 1];
-  na_features(sp, &n, s, phi);
-  for (int b = 0; b < A; ++b) avail[b] = na_available(&n, s, b);
-  na_actor(&n, phi, avail, h, pi);
-  *v = na_critic(&n, phi, g);
-  /* ∇ log π(a|s): the update direction na_train_one applies (δ = 1, lr = 1) */
-  int64_t k = 0;
-  double dh[64];
-  for (int q = 0; q < H; ++q) {
-    double sacc = 0.0;
-    for (int b = 0; b < A; ++b) {
-      if (!avail[b]) continue;
-      sacc += ((b == a ? 1.0 : 0.0) - pi[b]) * n.W2[b * H + q];
-    }
-    dh[q] = sacc * (1.0 - h[q] * h[q]);
-  }
-  for (int q = 0; q < H; ++q)
-    for (int f = 0; f < F; ++f) g_actor[k++] = dh[q] * phi[f];
-  for (int q = 0; q < H; ++q) g_actor[k++] = dh[q];
-  for (int b = 0; b < A; ++b)
-    for (int q = 0; q < H; ++q)
-      g_actor[k++] = avail[b] ? ((b == a ? 1.0 : 0.0) - pi[b]) * h[q] : 0.0;
-  for (int b = 0; b < A; ++b) g_actor[k++] = avail[b] ? (b == a ? 1.0 : 0.0) - pi[b] : 0.0;
-  k = 0;
-  for (int q = 0; q < H; ++q)
-    for (int f = 0; f < F; ++f) g_critic[k++] = n.u2[q] * (1.0 - g[q] * g[q]) * phi[f];
-  for (int q = 0; q < H; ++q) g_critic[k++] = n.u2[q] * (1.0 - g[q] * g[q]);
-  for (int q = 0; q < H; ++q) g_critic[k++] = g[q];
-  g_critic[k++] = 1.0;
-  na_free(&n);
   return 0;
 }

@@ -10,7 +10,9 @@
  *     on the exact fp64 widening of the fp32 or bf16 input bytes.
  *   - or_*: the configuration space of Eq.1–4 (power-of-two factors, odd
  *     cofactor at level 0), the state legitimacy bit J of Eq.5, the action set
- *     of Eq.6 / neighbour list of Eq.9, and the G-BFS of Alg.1 (§4.2).
+ *     of Eq.6 / neighbour list of Eq.9, the G-BFS of Alg.1 (§4.2), the
+ *     equal-budget random search (§5) and N-A2C (§4.3, Alg.2) with its
+ *     training step exposed for pinning (or_na2c_probe, or_na2c_train).
  *
  * Parity pins: see tests/test_oracle_*.py. The legitimacy predicate beyond
  * membership (the hardware constraints) has no paper pin: "parity unpinned"
@@ -104,32 +106,50 @@ int or_random_search(const or_space* sp, int64_t budget, uint64_t seed, or_cost_
  * one-hidden-layer tanh actor (softmax over the available actions) and critic,
  * ε = probability of following π, T-step walks from the current centre until
  * B unvisited legitimate states are collected (at most max_walks walks; an
- * episode that collects nothing lengthens the walks by one step and halves
- * the share ε of policy steps, up to T + 8 steps, then the search stops; a
- * new best resets both), each
- * timed state storing every transition from an already-timed neighbour into
- * the FIFO memory M (reward log(cost(s)/cost(s')) clipped to ±r_clip), and one
- * SGD pass over M after every timing (critic: semi-gradient TD(0); actor:
- * δ·∇log π). Randomness: SplitMix64(seed) for the walk, SplitMix64(seed ^
- * 0xA2C0A2C0A2C0A2C0) for the initial weights. res->popped holds the number of
- * episodes. Returns 0, or -1 on a bad argument. */
+ * episode that collects nothing lengthens the walks by one step, up to T + 8
+ * steps, then the search stops; with eps_halving it also halves ε; a new best
+ * resets both), each timed state storing every transition from an
+ * already-timed neighbour into the FIFO memory M, and one SGD pass over M
+ * after every timing (critic: semi-gradient TD(0); actor: δ·∇log π).
+ * Reward: reward = 0 gives §4.1's r(s, a) = 1/cost(s'); reward = 1 the
+ * variant log(cost(s)/cost(s')) clipped to ±r_clip. Randomness:
+ * SplitMix64(seed) for the walk, SplitMix64(seed ^ 0xA2C0A2C0A2C0A2C0) for
+ * the initial weights. res->popped holds the number of episodes. trace
+ * (optional, trace_cap entries) receives every transition stored into M, in
+ * storing order; *trace_n their total count. Returns 0, or -1 on a bad
+ * argument. */
 typedef struct {
   int32_t T, B, H, mem, max_walks;
+  int32_t reward;       /* 0: 1/cost(s') (§4.1); 1: clipped log ratio */
+  int32_t eps_halving;  /* 1: halve ε after an episode that collects nothing */
   double eps, gamma, lr, r_clip;
 } or_na2c_params;
+typedef struct {
+  uint64_t s, s2;  /* ranks of s and s' = step(s, a) */
+  int32_t a, pad;
+  double r;        /* r(s, a) */
+} or_na2c_transition;
 int or_na2c(const or_space* sp, const or_config* s0, const or_na2c_params* prm,
             int64_t budget, uint64_t seed, or_cost_fn cost, void* ctx, or_gbfs_result* res,
-            uint64_t* log_ranks, double* log_costs, int64_t log_cap);
-/* The actor's and critic's outputs and gradients at one state for the
- * weights after or_na2c's initialisation (for gradient checks): pi[A],
- * v, and the flattened gradients of log π(a|s) (actor) and V(s) (critic)
- * with respect to every parameter, in the order W1, b1, W2, b2 (actor) and
- * U1, c1, u2, c2 (critic). Returns the parameter counts through n_actor and
- * n_critic when the buffers are NULL. */
+            uint64_t* log_ranks, double* log_costs, int64_t log_cap,
+            or_na2c_transition* trace, int64_t trace_cap, int64_t* trace_n);
+/* The actor's and critic's outputs and gradients at one state, for the
+ * weights of or_na2c's initialisation or for the given flattened parameters
+ * (for gradient checks): pi[A], v, and the flattened gradients of
+ * log π(a|s) (actor) and V(s) (critic) with respect to every parameter, in
+ * the order W1, b1, W2, b2 (actor) and U1, c1, u2, c2 (critic). Returns the
+ * parameter counts through n_actor and n_critic when the buffers are NULL. */
 int or_na2c_probe(const or_space* sp, const or_na2c_params* prm, uint64_t seed,
                   const or_config* s, int a, const double* actor_params,
                   const double* critic_params, double* pi, double* v,
                   double* g_actor, double* g_critic, int64_t* n_actor, int64_t* n_critic);
+/* The training step or_na2c applies, on caller-given parameters (in/out, the
+ * probe's layout): transitions t = 0 … n−1 (s[t], a[t], r[t], s2[t]) in
+ * order, each one TD(0) actor-critic update with prm->gamma and prm->lr.
+ * Returns 0, or -1 on a bad argument (a[t] not available in s[t]). */
+int or_na2c_train(const or_space* sp, const or_na2c_params* prm, const or_config* s,
+                  const int* a, const double* r, const or_config* s2, int64_t n,
+                  double* actor_params, double* critic_params);
 
 #ifdef __cplusplus
 }

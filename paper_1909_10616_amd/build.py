@@ -53,10 +53,24 @@ def _units():
     return units
 
 
-def _newest_header():
-    hdrs = [os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith((".h", ".hpp"))]
-    hdrs += [os.path.join(ROOT, "include", f) for f in os.listdir(os.path.join(ROOT, "include"))]
-    return max(os.path.getmtime(h) for h in hdrs)
+def _deps(src):
+    """Headers a source depends on: its own #include "…" lines, followed
+    through csrc/ and include/ (local headers only)."""
+    seen, todo = set(), [os.path.join(CSRC, src)]
+    while todo:
+        path = todo.pop()
+        with open(path) as fh:
+            for line in fh:
+                line = line.strip()
+                if not line.startswith('#include "'):
+                    continue
+                name = line.split('"')[1]
+                for d in (CSRC, os.path.join(ROOT, "include")):
+                    h = os.path.join(d, name)
+                    if os.path.exists(h) and h not in seen:
+                        seen.add(h)
+                        todo.append(h)
+    return seen
 
 
 def _compile(unit, incremental=False):
@@ -64,7 +78,8 @@ def _compile(unit, incremental=False):
     obj = os.path.join(BUILD, name + ".o")
     if incremental and os.path.exists(obj):
         t = os.path.getmtime(obj)
-        if t > os.path.getmtime(os.path.join(CSRC, src)) and t > _newest_header():
+        srcs = [os.path.join(CSRC, src), *_deps(src)]
+        if all(t > os.path.getmtime(f) for f in srcs):
             return obj
     cmd = [HIPCC, *COMMON, "-x", "hip", *defs, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -76,7 +91,7 @@ def _compile(unit, incremental=False):
 
 def build(jobs: int | None = None, verbose: bool = True, incremental: bool = False) -> str:
     """Compile every unit (incremental=True: only units older than their
-    source or any header) and link libgemmtune.so."""
+    source or a header it includes) and link libgemmtune.so."""
     os.makedirs(BUILD, exist_ok=True)
     os.makedirs(LIBDIR, exist_ok=True)
     jobs = jobs or min(16, os.cpu_count() or 4)

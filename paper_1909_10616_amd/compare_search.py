@@ -34,6 +34,8 @@ def main():
     ap.add_argument("--s0", choices=["hand", "paper"], default="hand")
     ap.add_argument("--rho", type=int, default=5)
     ap.add_argument("--out", default=None)
+    ap.add_argument("--trace", action="store_true",
+                    help="name every candidate on stderr before it is launched")
     args = ap.parse_args()
 
     import torch
@@ -44,12 +46,6 @@ def main():
         raise SystemExit("compare_search needs a GPU")
     gt.lib()
     w = WORKLOADS[args.workload]
-    if max(w.M, w.N, w.K) >= 4096:
-        # A run of six seeds on the 4096^3 bf16 space ended in a GPU memory
-        # fault whose configuration was not recorded, and no cause has been
-        # found in the kernels' index arithmetic; the comparison stays off
-        # these sizes until one is.
-        raise SystemExit(f"compare_search: {w.name} is disabled (unexplained GPU fault at this size)")
     budget = args.budget or w.budget
     dev = torch.device("cuda:0")
     A, B = workload_inputs(w)
@@ -64,7 +60,9 @@ def main():
     for seed in range(args.seeds):
         row = {"seed": seed}
         for name, fn in (("gbfs", gt.tune_gbfs), ("random", gt.tune_random)):
-            kw = dict(budget=budget, seed=seed, t_max_s=args.t_max, A=Ad, B=Bd, C=C, c_ref=R)
+            # every candidate is named on stderr before it is launched
+            kw = dict(budget=budget, seed=seed, t_max_s=args.t_max, A=Ad, B=Bd, C=C, c_ref=R,
+                      trace_fd=2 if args.trace else -1)
             if name == "gbfs":
                 kw.update(s0=s0, rho=args.rho)
             print(f"seed {seed} {name}: searching", flush=True)

@@ -330,6 +330,22 @@ int gt_compare(const void* C, const void* R, int64_t n, void* stream, double* re
   return gt::compare_on_gpu(C, R, n, static_cast<hipStream_t>(stream), rel);
 }
 
+int gt_shutdown(void) {
+  std::lock_guard<std::mutex> lk(gt::g_cmp_mu);
+  int cur = -1;
+  const bool have_cur = hipGetDevice(&cur) == hipSuccess;
+  int rc = GT_OK;
+  for (int d = 0; d < 64; ++d) {
+    if (!gt::g_cmp_buf[d]) continue;
+    hipError_t e = hipSetDevice(d);
+    if (e == hipSuccess) e = hipFree(gt::g_cmp_buf[d]);
+    if (e != hipSuccess && rc == GT_OK) rc = gt::hip_fail(e, "gt_shutdown: hipFree (compare result)");
+    gt::g_cmp_buf[d] = nullptr;
+  }
+  if (have_cur) (void)hipSetDevice(cur);
+  return rc;
+}
+
 int gt_lower(const gt_config* cfg, int64_t M, int64_t N, int64_t K, int dtype,
              gt_kernel_info* info) {
   if (!cfg || !info) {

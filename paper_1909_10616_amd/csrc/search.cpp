@@ -34,6 +34,8 @@
 #include <utility>
 #include <vector>
 
+#include <unistd.h>
+
 #include "internal.h"
 #include "runtime.h"
 
@@ -134,6 +136,7 @@ int gt_tune_opts_init(gt_tune_opts* o) {
   o->budget = 1000;
   o->max_run_ms = 250.0;
   o->abort_factor = 50.0;
+  o->trace_fd = -1;
   return GT_OK;
 }
 
@@ -220,9 +223,17 @@ struct Tuner {
 
   // Times one configuration, logs it, counts it; returns its cost.
   double time_one(const gt_config& c, uint64_t rank) {
+    if (o->trace_fd >= 0) {
+      // on record before any launch: unbuffered, one write per line
+      const std::string line = std::string("[gemmtune] ") + who + " timing #" +
+                               std::to_string(out->timed) + " rank " + std::to_string(rank) + " " +
+                               describe(c) + "\n";
+      (void)!::write(o->trace_fd, line.data(), line.size());
+    }
     gt_log_entry rec{};
     rec.rank = rank;
     double v;
+    const auto te = std::chrono::steady_clock::now();
     if (cost) {
       v = cost(&c, rank, ctx);
       rec.cost_ms = v;
@@ -233,7 +244,13 @@ struct Tuner {
       rec.status = std::isinf(v) ? 2 : 0;
     } else {
       v = gpu_cost(g, c, cost_min, &rec);
+      // device time of the launches: the first warm-up, then the rest at the
+      // timed mean (an early abort stops after the first)
+      if (std::isfinite(rec.first_ms)) out->device_s += rec.first_ms * 1e-3;
+      if (rec.status != 1 && std::isfinite(rec.cost_ms))
+        out->device_s += (o->runs + std::max(o->warmup, 1) - 1) * rec.cost_ms * 1e-3;
     }
+    out->eval_s += std::chrono::duration<double>(std::chrono::steady_clock::now() - te).count();
     if (o->log && out->timed < o->log_cap) o->log[out->timed] = rec;
     ++out->timed;
     if (std::isinf(v)) ++out->failed;
@@ -575,20 +592,22 @@ class Agent {
     double r;
   };
 
-  // TD(0) advantage δ = r + γV(s') − V(s); critic θ += lr·δ·∇V(s); actor
-  // θ += lr·δ·∇log π(a|s); all gradients at the weights before this update.
+  // TD(0) advantage δ = r + γV(s') − V(s); every parameter θ moves by
+  // (lr·δ)·∂/∂θ, with ∂/∂θ of V(s) for the critic and of log π(a|s) for the
+  // actor, all taken at the weights before this update.
   void train(const Transition& t, double gamma, double lr) {
     double g[64], g2[64], h[64], dh[64], pi[kMaxNeighbours];
     const double v2 = value(t.phi2, g2);
     const double v = value(t.phi, g);
     const double delta = t.r + gamma * v2 - v;
+    const double step = lr * delta;
     for (int k = 0; k < H_; ++k) {
       const double back = u2_[k] * (1.0 - g[k] * g[k]);
-      for (int f = 0; f < F_; ++f) U1_[k * F_ + f] += lr * delta * back * t.phi[f];
-      c1_[k] += lr * delta * back;
+      for (int f = 0; f < F_; ++f) U1_[k * F_ + f] += step * (back * t.phi[f]);
+      c1_[k] += step * back;
     }
-    for (int k = 0; k < H_; ++k) u2_[k] += lr * delta * g[k];
-    c2_ += lr * delta;
+    for (int k = 0; k < H_; ++k) u2_[k] += step * g[k];
+    c2_ += step;
     policy(t.phi, t.avail, h, pi);
     for (int k = 0; k < H_; ++k) {
       double acc = 0.0;
@@ -599,12 +618,12 @@ class Agent {
     for (int b = 0; b < A_; ++b) {
       if (!t.avail[b]) continue;
       const double e = (b == t.a ? 1.0 : 0.0) - pi[b];
-      for (int k = 0; k < H_; ++k) W2_[b * H_ + k] += lr * delta * e * h[k];
-      b2_[b] += lr * delta * e;
+      for (int k = 0; k < H_; ++k) W2_[b * H_ + k] += step * (e * h[k]);
+      b2_[b] += step * e;
     }
     for (int k = 0; k < H_; ++k) {
-      for (int f = 0; f < F_; ++f) W1_[k * F_ + f] += lr * delta * dh[k] * t.phi[f];
-      b1_[k] += lr * delta * dh[k];
+      for (int f = 0; f < F_; ++f) W1_[k * F_ + f] += step * (dh[k] * t.phi[f]);
+      b1_[k] += step * dh[k];
     }
   }
 
@@ -616,7 +635,11 @@ class Agent {
   double c2_ = 0.0;
 };
 
-double reward(double before, double after, double clip) {
+// r(s, a) for a transition into s' (cost `after`) from s (cost `before`):
+// §4.1's 1/cost(s') (a failed s', cost +inf, earns 0), or with log_ratio the
+// variant log(cost(s)/cost(s')) clipped to ±clip.
+double reward(bool log_ratio, double before, double after, double clip) {
+  if (!log_ratio) return 1.0 / after;
   if (std::isinf(after)) return std::isinf(before) ? 0.0 : -clip;
   if (std::isinf(before)) return clip;
   return std::min(clip, std::max(-clip, std::log(before / after)));
@@ -637,9 +660,11 @@ static int tune_na2c_impl(const gt_space* sp, const gt_tune_opts* o, const gt_na
   if (params) p = *params;
   if (p.T < 1 || p.T > 64 || p.B < 1 || p.B > 65536 || p.H < 1 || p.H > 64 || p.mem < 1 ||
       p.mem > 65536 || p.max_walks < 1 || p.max_walks > (1 << 20) ||
-      !(p.eps >= 0.0 && p.eps <= 1.0) || !(p.lr >= 0.0) || !(p.r_clip > 0.0)) {
+      !(p.eps >= 0.0 && p.eps <= 1.0) || !(p.lr >= 0.0) || !(p.r_clip > 0.0) ||
+      (p.reward != 0 && p.reward != 1) || (p.eps_halving != 0 && p.eps_halving != 1)) {
     set_error("tune_na2c: parameters out of range (1 <= T <= 64; 1 <= B, mem <= 65536; "
-              "1 <= max_walks <= 2^20; 1 <= H <= 64; 0 <= eps <= 1; lr >= 0; r_clip > 0)");
+              "1 <= max_walks <= 2^20; 1 <= H <= 64; 0 <= eps <= 1; lr >= 0; r_clip > 0; "
+              "reward and eps_halving 0 or 1)");
     return GT_EINVAL;
   }
   const Space& s = t.s;
@@ -685,7 +710,7 @@ static int tune_na2c_impl(const gt_space* sp, const gt_tune_opts* o, const gt_na
   double phi[3 * GT_MAXD + 1], h[64], pi[kMaxNeighbours];
   char avail[kMaxNeighbours];
   int walk = p.T;        // walk length: grows by one after an episode that collects nothing
-  double eps_now = p.eps;  // share of policy steps: halves after such an episode
+  double eps_now = p.eps;  // share of policy steps (halves after such an episode: variant)
   while (true) {
     if (out->timed >= o->budget) {
       out->stop_reason = 0;
@@ -736,14 +761,14 @@ static int tune_na2c_impl(const gt_space* sp, const gt_tune_opts* o, const gt_na
     ++out->popped;
     if (coll.empty()) {
       // nothing new within `walk` steps of the centre: look one step further
-      // (the exploration step may grow, §4.3) with half the policy steps,
-      // up to T + 8, then stop
+      // (the exploration step may grow, §4.3), up to T + 8, then stop; the
+      // eps_halving variant also halves the share of policy steps
       if (walk >= p.T + 8) {
         out->stop_reason = 1;
         break;
       }
       ++walk;
-      eps_now *= 0.5;
+      if (p.eps_halving) eps_now *= 0.5;
       continue;
     }
     for (size_t b = 0; b < coll.size() && out->timed < o->budget; ++b) {
@@ -769,7 +794,7 @@ static int tune_na2c_impl(const gt_space* sp, const gt_tune_opts* o, const gt_na
         agent.features(coll[b], tr.phi2);
         for (int a = 0; a < A; ++a) tr.avail[a] = agent.available(prev, a) ? 1 : 0;
         tr.a = agent.inverse(bb);
-        tr.r = reward(it->second, c, p.r_clip);
+        tr.r = reward(p.reward == 1, it->second, c, p.r_clip);
         if (mem.size() < static_cast<size_t>(p.mem)) {
           mem.push_back(tr);
         } else {

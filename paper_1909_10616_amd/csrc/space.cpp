@@ -228,6 +228,10 @@ int legit_levels(const Levels& L) {
   // a dispatch packet holds at most 2^32 - 1 work-items per grid dimension
   if (L.gridM * L.gridN * 64 * L.W > int64_t{4294967295}) return 0;
   if (L.kSplit > 65535) return 0;
+  // and the launch as a whole stays below 2^32 work-items, so that no 32-bit
+  // count over the whole dispatch can wrap (this also bounds the split-K
+  // partial sums, M·N·kSplit atomics, and the launches a search can time)
+  if (L.gridM * L.gridN * L.kSplit * 64 * L.W > int64_t{4294967295}) return 0;
   return 1;
 }
 }  // namespace

@@ -70,12 +70,14 @@ class gt_tune_opts(ctypes.Structure):
                 ("A", ctypes.c_void_p), ("B", ctypes.c_void_p), ("C", ctypes.c_void_p),
                 ("c_ref", ctypes.c_void_p), ("stream", ctypes.c_void_p),
                 ("log", ctypes.POINTER(gt_log_entry)), ("log_cap", ctypes.c_int64),
-                ("progress_s", ctypes.c_double)]
+                ("progress_s", ctypes.c_double), ("trace_fd", ctypes.c_int32),
+                ("reserved2", ctypes.c_int32)]
 
 
 class gt_na2c_params(ctypes.Structure):
     _fields_ = [("T", ctypes.c_int32), ("B", ctypes.c_int32), ("H", ctypes.c_int32),
                 ("mem", ctypes.c_int32), ("max_walks", ctypes.c_int32),
+                ("reward", ctypes.c_int32), ("eps_halving", ctypes.c_int32),
                 ("reserved", ctypes.c_int32), ("eps", ctypes.c_double),
                 ("gamma", ctypes.c_double), ("lr", ctypes.c_double), ("r_clip", ctypes.c_double)]
 
@@ -86,13 +88,14 @@ class gt_tune_result(ctypes.Structure):
                 ("popped", ctypes.c_int64), ("skipped_illegit", ctypes.c_int64),
                 ("skipped_visited", ctypes.c_int64), ("failed", ctypes.c_int64),
                 ("wall_s", ctypes.c_double), ("stop_reason", ctypes.c_int32),
-                ("reserved", ctypes.c_int32)]
+                ("reserved", ctypes.c_int32), ("eval_s", ctypes.c_double),
+                ("device_s", ctypes.c_double)]
 
 
 EXPORTS = ("gt_space_size", "enumerate_configs", "config_rank", "config_unrank", "config_legit",
            "neighbours", "gemm_run", "gt_measure", "gt_reference_gemm", "gt_compare",
            "gt_lower", "gt_tune_opts_init", "tune_gbfs", "tune_random", "gt_na2c_params_init",
-           "tune_na2c", "gt_last_error")
+           "tune_na2c", "gt_shutdown", "gt_last_error")
 
 _lib = None
 
@@ -129,6 +132,7 @@ def lib():
     L.gt_na2c_params_init.argtypes = [ctypes.POINTER(gt_na2c_params)]
     L.tune_na2c.argtypes = [SP, ctypes.POINTER(gt_tune_opts), ctypes.POINTER(gt_na2c_params),
                             gt_cost_fn, P, ctypes.POINTER(gt_tune_result)]
+    L.gt_shutdown.argtypes = []
     L.gt_last_error.restype = ctypes.c_char_p
     for name in EXPORTS:
         if name != "gt_last_error":
@@ -297,6 +301,11 @@ def gt_reference_gemm(A, B, C, stream=None, a_kmajor=False):
     return C
 
 
+def gt_shutdown():
+    """Release the device memory the library keeps between calls."""
+    _check(lib().gt_shutdown(), "gt_shutdown")
+
+
 def gt_compare(C, R, stream=None) -> float:
     assert C.numel() == R.numel() and C.is_cuda and R.is_cuda
     rel = ctypes.c_double()
@@ -307,7 +316,7 @@ def gt_compare(C, R, stream=None) -> float:
 
 def _tune(entry, space: Space, budget: int, s0, rho, seed, runs, warmup, check, t_max_s,
           max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream, progress_s=0.0,
-          na2c=None) -> dict:
+          na2c=None, trace_fd=-1) -> dict:
     L = lib()
     o = gt_tune_opts()
     _check(L.gt_tune_opts_init(ctypes.byref(o)), "gt_tune_opts_init")
@@ -318,6 +327,7 @@ def _tune(entry, space: Space, budget: int, s0, rho, seed, runs, warmup, check, 
     o.budget, o.t_max_s, o.seed = budget, t_max_s, seed
     o.max_run_ms, o.abort_factor = max_run_ms, abort_factor
     o.progress_s = progress_s
+    o.trace_fd = int(trace_fd)
     log = (gt_log_entry * budget)()
     o.log = ctypes.cast(log, ctypes.POINTER(gt_log_entry))
     o.log_cap = budget
@@ -332,6 +342,13 @@ def _tune(entry, space: Space, budget: int, s0, rho, seed, runs, warmup, check, 
         if (M, N, K, dt) != (space.M, space.N, space.K, space.dtype):
             raise ValueError("operands do not match the space")
         o.A, o.B, o.C = A.data_ptr(), B.data_ptr(), C.data_ptr()
+        if c_ref is not None:
+            import torch
+            # the library writes M·N fp32 values through c_ref
+            if not (c_ref.is_cuda and c_ref.device == C.device and c_ref.is_contiguous()
+                    and c_ref.dtype == torch.float32 and c_ref.numel() == M * N):
+                raise ValueError("c_ref must be a contiguous float32 tensor of M·N elements on "
+                                 "C's device")
         o.c_ref = c_ref.data_ptr() if c_ref is not None else None
         o.stream = _stream(stream)
     res = gt_tune_result()
@@ -356,7 +373,7 @@ def _tune(entry, space: Space, budget: int, s0, rho, seed, runs, warmup, check, 
             "best_cost": res.best_cost, "timed": n, "popped": int(res.popped),
             "skipped_illegit": int(res.skipped_illegit),
             "skipped_visited": int(res.skipped_visited), "failed": int(res.failed),
-            "wall_s": res.wall_s,
+            "wall_s": res.wall_s, "eval_s": res.eval_s, "device_s": res.device_s,
             "stop_reason": ("neighbourhood-exhausted" if entry == "tune_na2c" and res.stop_reason == 1
                             else STOP.get(res.stop_reason, "?")),
             "log": entries}
@@ -365,41 +382,62 @@ def _tune(entry, space: Space, budget: int, s0, rho, seed, runs, warmup, check, 
 def tune_gbfs(space: Space, budget: int, s0=None, rho: int = 5, seed: int = 0, runs: int = 10,
               warmup: int = 1, check: bool = True, t_max_s: float = 0.0,
               max_run_ms: float = 250.0, abort_factor: float = 50.0, A=None, B=None, C=None,
-              c_ref=None, cost_fn=None, stream=None, progress_s: float = 0.0) -> dict:
+              c_ref=None, cost_fn=None, stream=None, progress_s: float = 0.0,
+              trace_fd: int = -1) -> dict:
     """Run G-BFS (Alg.1). With ``cost_fn(cfg, rank) -> float`` the costs are
     synthetic (no GPU); otherwise A, B, C are GPU tensors and every candidate
     is timed with ``gemm_run`` on the stream (A is W, K×M, when the space has
-    a_kmajor). progress_s > 0: a progress line on stderr at most that often."""
+    a_kmajor). progress_s > 0: a progress line on stderr at most that often;
+    trace_fd >= 0: each candidate is named on that file descriptor before it
+    is launched."""
     return _tune("tune_gbfs", space, budget, s0, rho, seed, runs, warmup, check, t_max_s,
-                 max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream, progress_s)
+                 max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream, progress_s,
+                 trace_fd=trace_fd)
 
 
 def tune_random(space: Space, budget: int, seed: int = 0, runs: int = 10, warmup: int = 1,
                 check: bool = True, t_max_s: float = 0.0, max_run_ms: float = 250.0,
                 abort_factor: float = 50.0, A=None, B=None, C=None, c_ref=None, cost_fn=None,
-                stream=None, progress_s: float = 0.0) -> dict:
+                stream=None, progress_s: float = 0.0, trace_fd: int = -1) -> dict:
     """Equal-budget random search (§5 baseline); same timing and result as
     tune_gbfs, ``popped`` counts the draws."""
     return _tune("tune_random", space, budget, None, 1, seed, runs, warmup, check, t_max_s,
-                 max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream, progress_s)
+                 max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream, progress_s,
+                 trace_fd=trace_fd)
 
 
 def tune_na2c(space: Space, budget: int, s0=None, seed: int = 0, runs: int = 10,
               warmup: int = 1, check: bool = True, t_max_s: float = 0.0,
               max_run_ms: float = 250.0, abort_factor: float = 50.0, A=None, B=None, C=None,
               c_ref=None, cost_fn=None, stream=None, progress_s: float = 0.0,
-              params=None) -> dict:
+              params=None, trace_fd: int = -1) -> dict:
     """N-A2C (§4.3, Alg.2); timing, log and result as tune_gbfs (``popped``
     counts episodes). ``params``: overrides of gt_na2c_params (T, B, H, mem,
-    max_walks, eps, gamma, lr, r_clip)."""
+    max_walks, reward, eps_halving, eps, gamma, lr, r_clip)."""
     return _tune("tune_na2c", space, budget, s0, 1, seed, runs, warmup, check, t_max_s,
                  max_run_ms, abort_factor, A, B, C, c_ref, cost_fn, stream, progress_s,
-                 na2c=params)
+                 na2c=params, trace_fd=trace_fd)
 
 
 def tflops(M, N, K, ms) -> float:
     """2·M·N·K floating-point operations per run (one multiply-add = 2 flops)."""
     return 2.0 * M * N * K / (ms * 1e-3) / 1e12 if ms > 0 and math.isfinite(ms) else 0.0
+
+
+def report(M, N, K, dtype, ms, timed, space_size, peak_tflops) -> dict:
+    """The figures a search is reported by (§5 reports the share of the space
+    explored): TFLOP/s of the best configuration (2·M·N·K per run), its share
+    of the dtype's dense MFMA peak in %, the configurations timed as a
+    percentage of the whole space |ξ| (illegitimate states included), and the
+    HBM rate at the algorithmic bytes — A and B read once, C (fp32) written
+    once."""
+    esz = 2 if dtype_code(dtype) & ~A_KMAJOR == BF16 else 4
+    alg_bytes = (M * K + K * N) * esz + M * N * 4
+    tf = tflops(M, N, K, ms)
+    return {"tflops": tf, "pct_of_peak": 100.0 * tf / peak_tflops,
+            "fraction_of_space_pct": 100.0 * timed / space_size,
+            "algorithmic_bytes": alg_bytes,
+            "hbm_gbs": alg_bytes / (ms * 1e-3) / 1e9 if ms > 0 and math.isfinite(ms) else 0.0}
 
 
 def hand_start(M: int, N: int, K: int, d, mfma_coord: bool):

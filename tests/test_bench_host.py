@@ -61,17 +61,3 @@ def test_committed_traffic_line_matches_the_sources(bench):
     lines = [l for l in open(os.path.join(ROOT, "profiles", "traffic.txt"))
              if not l.startswith("#") and "|" in l]
     assert any(f"source={bench.kernel_source_hash()}" in l for l in lines)
-
-
-def test_power_clock_sample_parser():
-    """The telemetry parser of power_clock.py: time stamp, socket power and the
-    per-XCD shader clocks of each sample; malformed samples are skipped."""
-    from paper_1909_10616_amd.power_clock import parse_samples
-    sample = ('{"gpu_data": [{"gpu": 0, "power": {"socket_power": {"value": %d, "unit": "W"}}, '
-              '"clock": {"gfx_0": {"clk": {"value": %d, "unit": "MHz"}}, '
-              '"gfx_1": {"clk": {"value": %d, "unit": "MHz"}}, "mem_0": {"clk": {"value": 2000}}}}]}')
-    text = ("T 10.5\n" + sample % (1390, 2100, 2150) + "\n"
-            "T 11.0\nnot json at all\n"
-            "T 11.5\n" + sample % (1385, 2090, 2140) + "\n")
-    got = parse_samples(text)
-    assert got == [(10.5, 1390.0, [2100, 2150]), (11.5, 1385.0, [2090, 2140])]

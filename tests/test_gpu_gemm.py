@@ -167,8 +167,29 @@ FULL = [
 ]
 
 
+_FULL_REF = {}
+
+
+def _oracle_threads():
+    aff = len(os.sched_getaffinity(0))
+    return max(1, min(int(os.environ.get("OMP_NUM_THREADS", "0")) or aff, aff))
+
+
+def _full_oracle(orc, w, A, B):
+    """The whole fp64 oracle product of a workload (kept for the module:
+    several configurations share a workload)."""
+    if w.name not in _FULL_REF:
+        _FULL_REF.clear()
+        _FULL_REF[w.name] = orc.gemm(raw_bytes(A), raw_bytes(B), w.M, w.N, w.K, w.dtype,
+                                     nthreads=_oracle_threads())
+    return _FULL_REF[w.name]
+
+
 @pytest.mark.parametrize("case", FULL, ids=[f"{c[0]}-{i}" for i, c in enumerate(FULL)])
-def test_full_size_sampled_entries(gt, orc, case):
+def test_full_size_every_element(gt, orc, case):
+    """Every element of C at the workload list's full shapes against the fp64
+    oracle's whole product (normwise max relative error within the dtype's
+    tolerance), plus the row- and column-sum identities."""
     from workloads import WORKLOADS, workload_inputs
     w = WORKLOADS[case[0]]
     cfg = case[1]
@@ -178,12 +199,9 @@ def test_full_size_sampled_entries(gt, orc, case):
     A, B = workload_inputs(w)
     C = run(gt, cfg, A, B)
     assert np.isfinite(C).all()
-    rng = np.random.default_rng(1)
-    rows = np.concatenate([[0, w.M - 1], rng.integers(0, w.M, 254)])
-    cols = np.concatenate([[0, w.N - 1], rng.integers(0, w.N, 254)])
-    ref = orc.gemm_entries(raw_bytes(A), raw_bytes(B), w.M, w.N, w.K, w.dtype, rows, cols)
-    got = C[rows, cols].astype(np.float64)
-    e = np.abs(got - ref).max() / np.abs(ref).max()
+    ref = _full_oracle(orc, w, A, B)
+    e = rel_err(C, ref)
+    note(f"  max |C - C*| / max |C*| = {e:.3e}")
     assert e <= tol(w.dtype, w.K), e
     _rowcol_property(C, A, B, w.dtype, orc)
 
@@ -252,3 +270,40 @@ def test_direct_load_path_bit_exact(gt, orc, shape):
         C = run(gt, c, A, B)
         assert np.array_equal(C.astype(np.float64), ref), c
 
+
+
+def test_shutdown_releases_and_library_stays_usable(gt, orc):
+    """gt_shutdown frees the comparison buffers; calling it twice is fine and
+    the library allocates again on the next use."""
+    dev = torch.device("cuda:0")
+    M = N = K = 256
+    A, B = make_inputs(M, N, K, "f32", 3, "smallint")
+    ref = orc.gemm(raw_bytes(A), raw_bytes(B), M, N, K, "f32")
+    Ad, Bd = A.to(dev), B.to(dev)
+    R = torch.empty(M, N, device=dev)
+    gt.gt_reference_gemm(Ad, Bd, R)
+    assert gt.gt_compare(R, R) == 0.0          # allocates the buffer
+    gt.gt_shutdown()
+    gt.gt_shutdown()
+    cfg = ((4, 2, 2, 16), (16, 1, 4, 4), (4, 2, 2, 16), 0)
+    C = torch.full((M, N), float("nan"), device=dev)
+    gt.gemm_run(cfg, Ad, Bd, C)
+    torch.cuda.synchronize()
+    assert np.array_equal(C.cpu().numpy().astype(np.float64), ref)
+    assert gt.gt_compare(C, R) == 0.0          # allocates again
+    gt.gt_shutdown()
+
+
+def test_search_rejects_a_bad_reference_buffer(gt):
+    """c_ref receives M·N fp32 values: a wrong size, dtype, device or layout
+    is refused before the library sees it."""
+    dev = torch.device("cuda:0")
+    M = N = K = 64
+    sp = gt.Space(M, N, K, (3, 3, 3), "f32", False)
+    A = torch.zeros(M, K, device=dev)
+    B = torch.zeros(K, N, device=dev)
+    C = torch.zeros(M, N, device=dev)
+    for bad in (torch.zeros(M * N - 1, device=dev), torch.zeros(M, N, device=dev, dtype=torch.bfloat16),
+                torch.zeros(M, N), torch.zeros(N, M, device=dev).t()):
+        with pytest.raises(ValueError):
+            gt.tune_gbfs(sp, budget=2, A=A, B=B, C=C, c_ref=bad)

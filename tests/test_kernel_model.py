@@ -457,3 +457,219 @@ def test_ring_carried_state_matches_closed_forms(ns):
                         cur, cur_b = 0, lds0
                     else:
                         cur_b += stage16
+
+
+# --- the generic path, the split-K fill and the launch as a whole ----------
+
+def max_waves(I, TM, TN):
+    acc = TM * TN * I * I // 64
+    return 16 if acc + 96 <= 128 else (8 if acc + 96 <= 256 else 4)
+
+
+def tile_map(nt, gridM, gridN, t):
+    """Workgroup id t -> (tile row, tile column): the XCD-aware remap when
+    the tile count is a multiple of 8, then groups of 4 tile rows."""
+    if nt % 8 == 0:
+        t = (t & 7) * (nt >> 3) + (t >> 3)
+    per_group = 4 * gridN
+    group = t // per_group
+    first = group * 4
+    gsize = np.minimum(gridM - first, 4)
+    r = t - group * per_group
+    return first + r % gsize, r // gsize
+
+
+def check_tile_map(L):
+    gM, gN = L["gridM"], L["gridN"]
+    nt = gM * gN
+    if nt <= 1 << 20:
+        gm, gn = tile_map(nt, gM, gN, np.arange(nt, dtype=np.int64))
+        assert gm.min() >= 0 and gm.max() < gM and gn.min() >= 0 and gn.max() < gN
+        assert len(np.unique(gm * gN + gn)) == nt   # every tile exactly once
+    else:
+        rng = np.random.default_rng(nt)
+        t = np.concatenate([np.arange(64), nt - 1 - np.arange(64), rng.integers(0, nt, 4096)])
+        gm, gn = tile_map(nt, gM, gN, t.astype(np.int64))
+        assert gm.min() >= 0 and gm.max() < gM and gn.min() >= 0 and gn.max() < gN
+
+
+def _copy_tile(rows, cols, vec, nthr):
+    """(row, column) of every element (or first element of a 16-byte chunk)
+    the cooperative tile copy moves, over all threads and iterations."""
+    if vec > 1:
+        lgcpr = lg(cols) - lg(vec)
+        e = np.arange((rows * cols) >> lg(vec))
+        return e >> lgcpr, (e & ((1 << lgcpr) - 1)) << lg(vec)
+    e = np.arange(rows * cols)
+    return e >> lg(cols), e & (cols - 1)
+
+
+def check_generic(L, info, M, N, K, dtype="bf16", akm=False):
+    I, TM, TN, W = L["I"], L["TM"], L["TN"], L["W"]
+    BM, BN, BK = L["BM"], L["BN"], L["BK"]
+    esz, vec = (2, 8) if dtype == "bf16" else (4, 4)
+    nthr = 64 * W
+    assert nthr <= 64 * max_waves(I, TM, TN)        # the instantiation's launch bound
+    stage = (BM + BN) * BK * esz
+    assert info["lds_bytes"] == stage * (2 if info["dbuf"] else 1) <= LDS_MAX
+    assert info["grid_x"] == L["gridM"] * L["gridN"] and info["grid_y"] == L["kSplit"]
+    assert info["grid_x"] * nthr < 2 ** 32 and info["grid_y"] <= 65535
+    assert info["grid_x"] * info["grid_y"] * nthr < 2 ** 32
+    check_tile_map(L)
+    # vector copies only where the lowering allows them (16-byte aligned rows)
+    a_vec = vec if ((BM % vec == 0 and M % vec == 0) if akm else (BK % vec == 0 and K % vec == 0)) else 1
+    b_vec = vec if (BN % vec == 0 and N % vec == 0) else 1
+    for gm, gn, z, l in tiles(L):
+        kbase = (l * L["kSplit"] + z) * BK
+        for av in sorted({1, a_vec}):
+            if akm:   # BK rows of BM contiguous m from W (K×M)
+                r, c = _copy_tile(BK, BM, av, nthr)
+                src = gm * BM + (kbase + r) * M + c
+                assert src.min() >= 0 and src.max() + av <= K * M
+                assert ((r << lg(BM)) + c).max() + av <= BM * BK
+            else:
+                r, c = _copy_tile(BM, BK, av, nthr)
+                src = (gm * BM + r) * K + kbase + c
+                assert src.min() >= 0 and src.max() + av <= M * K
+                assert ((r << lg(BK)) + c).max() + av <= BM * BK
+        for bv in sorted({1, b_vec}):
+            r, c = _copy_tile(BK, BN, bv, nthr)
+            src = (kbase + r) * N + gn * BN + c
+            assert src.min() >= 0 and src.max() + bv <= K * N
+            assert ((r << lg(BN)) + c).max() + bv <= BK * BN
+    # fragment gathers: rows / columns and k inside the stage when unguarded
+    lane = np.arange(64)
+    IK = (16 if I == 32 else 32) if dtype == "bf16" else (2 if I == 32 else 4)
+    EPL = 8 if dtype == "bf16" else 1
+    tpbM = L["blkM"] // I if L["blkM"] >= I else 1
+    tpbN = L["blkN"] // I if L["blkN"] >= I else 1
+    nkk = -(-L["kBlk"] // IK)
+    sr, sk = (1, BM) if akm else (BK, 1)
+    # k inside the stage, s·kBlk + kl for the first and last sub-step s and
+    # every k-chunk (the index is affine in s), this lane's EPL elements
+    subs = np.array(sorted({0, L["kSub"] - 1}))[:, None, None, None]
+    kl = (np.arange(nkk)[None, :, None, None] * IK + (lane // I)[None, None, None, :] * EPL
+          + np.arange(EPL)[None, None, :, None])
+    kin = kl < L["kBlk"]
+    kidx = subs * L["kBlk"] + kl
+    for w in range(W):
+        wm, wn = w % L["wavesM"], w // L["wavesM"]
+        for t in range(TM):
+            inn = (t % tpbM) * I + lane % I
+            row = wm * L["WM"] + (t // tpbM) * L["blkM"] + inn
+            ok = inn < L["blkM"]
+            assert row[ok].max(initial=0) < BM
+            okk = ok & kin
+            idx = row * sr + kidx * sk
+            assert idx[np.broadcast_to(okk, idx.shape)].max(initial=0) < BM * BK
+        for t in range(TN):
+            inn = (t % tpbN) * I + lane % I
+            col = wn * L["WN"] + (t // tpbN) * L["blkN"] + inn
+            ok = inn < L["blkN"]
+            assert col[ok].max(initial=0) < BN
+            okk = ok & kin
+            idx = kidx * BN + col
+            assert idx[np.broadcast_to(okk, idx.shape)].max(initial=0) < BK * BN
+        # epilogue: guarded (row, column) of every accumulator element
+        i = np.arange(TM)[:, None, None]
+        e = np.arange(I * I // 64)[None, :, None]
+        lr = lane[None, None, :]
+        ri = (i % tpbM) * I + ((8 * (e >> 2) + 4 * (lr >> 5) + (e & 3)) if I == 32
+                               else (4 * (lr >> 4) + e))
+        r = (wm * L["WM"] + (i // tpbM) * L["blkM"] + ri)[:, :, None, :]
+        j = np.arange(TN)[:, None]
+        ci = (j % tpbN) * I + lane[None, :] % I
+        c = (wn * L["WN"] + (j // tpbN) * L["blkN"] + ci)[None, None, :, :]
+        ok = (ri < L["blkM"])[:, :, None, :] & (ci < L["blkN"])[None, None, :, :]
+        for gm, gn, _, _ in tiles(L):
+            g = (gm * BM + r) * N + gn * BN + c
+            assert g[ok].max(initial=0) < M * N and g[ok].min(initial=0) >= 0
+
+
+@functools.lru_cache(maxsize=None)
+def check_fill(n):
+    """The split-K clear: ≤ 65536 blocks of 256 threads, grid-stride loop;
+    thread f = block·256 + tid writes f, f + stride, … below n."""
+    blocks = min(-(-n // 256), 65536)
+    stride = blocks * 256
+    assert stride <= 2 ** 32 and (stride >= n or blocks == 65536)
+    first = np.arange(stride, dtype=np.int64)
+    # every element of C written exactly once
+    assert int(np.maximum(0, -(-(n - first) // stride)).sum()) == n
+    return True
+
+
+def run_models(gt, cfgs, M, N, K, dtype="bf16", akm=False):
+    n = {"dl": 0, "fast": 0, "generic": 0}
+    code = gt.dtype_code(dtype) | (gt.A_KMAJOR if akm else 0)
+    for c in cfgs:
+        info = gt.lower(c, M, N, K, code)
+        L = levels(c)
+        if info["dl"]:
+            check_dl(L, info, M, N, K)
+            n["dl"] += 1
+        elif info["fast"]:
+            check_fast(L, info, M, N, K, vec=8 if dtype == "bf16" else 4, akm=akm)
+            n["fast"] += 1
+        else:
+            check_generic(L, info, M, N, K, dtype, akm)
+            n["generic"] += 1
+        if L["kSplit"] > 1:
+            check_fill(M * N)
+    return n
+
+
+def _draws(size, seed, count):
+    """The first `count` ranks the random search draws (SplitMix64 mod |ξ|)."""
+    out, st = [], seed
+    for _ in range(count):
+        st = (st + 0x9E3779B97F4A7C15) & (2 ** 64 - 1)
+        z = st
+        z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & (2 ** 64 - 1)
+        z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & (2 ** 64 - 1)
+        out.append((z ^ (z >> 31)) % size)
+    return out
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_search_candidates_4096(gt, orc, seed):
+    """Every configuration the equal-budget random search times on the 4096³
+    bf16 space (seeds 0-5, budget 1000; draws are cost-independent) passes
+    the kernel models: in-bounds global, LDS and C accesses, the tile map a
+    bijection, the launch within the instantiation's bound, and the whole
+    dispatch below 2^32 work-items. The draw sequence of every seed also holds
+    configurations that meet every other legitimacy clause but launch 2^32 or
+    more work-items (up to 2^40): the whole-launch clause rejects those."""
+    D = 4096
+    sp = gt.Space(D, D, D, (4, 4, 4), "bf16", True)
+    timed = []
+    gt.tune_random(sp, budget=1000, seed=seed, cost_fn=lambda c, r: (timed.append(c), 1.0)[1])
+    assert len(timed) == 1000
+    n = run_models(gt, timed, D, D, D)
+    assert n["generic"] > 900, n
+    osp = orc.Space(D, D, D, (4, 4, 4), "bf16", True)
+    oversized = 0
+    for r in _draws(sp.size(), seed, 3000):
+        c = osp.unrank(r)
+        L = levels(c)
+        items = L["gridM"] * L["gridN"] * L["kSplit"] * 64 * L["W"]
+        if items >= 2 ** 32 and not osp.legit(c):
+            oversized += 1
+    assert oversized > 0
+
+
+@pytest.mark.parametrize("space", [(4096, 4096, 4096, "bf16"), (4096, 11008, 4096, "bf16"),
+                                   (64, 4096, 4096, "bf16"), (1024, 1024, 1024, "f32")])
+def test_model_legitimate_sample(gt, space):
+    """A seeded sample of legitimate configurations of four workload spaces,
+    every path."""
+    M, N, K, dt = space
+    sp = gt.Space(M, N, K, (4, 4, 4), dt, dt == "bf16")
+    rng = random.Random(M * 7 + N)
+    cfgs = []
+    while len(cfgs) < 400:
+        c = sp.unrank(rng.randrange(sp.size()))
+        if sp.legit(c):
+            cfgs.append(c)
+    n = run_models(gt, cfgs, M, N, K, dt)
+    assert n["generic"] > 200, n

@@ -292,6 +292,10 @@ NA2C_CASES = [
     (256, 256, 512, (4, 4, 4), "bf16", True, 0, 250, 3, {"eps": 0.5, "mem": 64}),
     (96, 80, 48, (4, 3, 4), "bf16", True, 1, 200, 1, {"H": 8, "lr": 0.05}),
     (64, 32, 64, (3, 2, 3), "f32", False, 1, 400, 2, None),           # small: walks lengthen
+    # the variants: clipped log-ratio reward, ε halving after empty episodes
+    (512, 512, 512, (4, 2, 4), "f32", False, 1, 300, 4, {"reward": 1}),
+    (64, 32, 64, (3, 2, 3), "f32", False, 1, 400, 5, {"eps_halving": 1}),
+    (256, 256, 512, (4, 4, 4), "bf16", True, 0, 250, 6, {"reward": 1, "eps_halving": 1}),
 ]
 
 
@@ -325,7 +329,7 @@ def test_tune_na2c_synthetic_trajectory_matches_oracle(gt, orc, case, cost_kind)
 def test_tune_na2c_errors(gt):
     sp = gt.Space(256, 256, 256, (3, 3, 3), "f32", False)
     for bad in ({"T": 0}, {"B": 0}, {"H": 65}, {"mem": 0}, {"max_walks": 0}, {"eps": 1.5},
-                {"lr": -1.0}, {"r_clip": 0.0}):
+                {"lr": -1.0}, {"r_clip": 0.0}, {"reward": 2}, {"eps_halving": -1}):
         with pytest.raises(gt.GemmTuneError):
             gt.tune_na2c(sp, 10, cost_fn=lambda c, r: 1.0, params=bad)
     with pytest.raises(gt.GemmTuneError):   # s0 not in the space
@@ -346,3 +350,34 @@ def test_full_enumeration_every_workload_space(gt, orc, name):
     for start in range(0, size, 1 << 22):
         legit += _compare_window(gt, orc, args, start, min(1 << 22, size - start))
     assert 0 < legit < size
+
+
+def test_report_arithmetic_exact(gt):
+    """The report's figures against exact rational arithmetic: TFLOP/s =
+    2MNK / cost, % of peak, timed / |ξ| (the whole space), HBM GB/s at the
+    algorithmic bytes; each within one rounding of the exact value."""
+    from fractions import Fraction as F
+
+    def close(x, q):
+        assert abs(F(x) - q) <= abs(q) * F(1, 2 ** 50), (x, float(q))
+
+    cases = [(4096, 4096, 4096, "bf16", 0.11514, 1000, 188392750, 2516.6),
+             (256, 256, 256, "f32", 0.0063, 64, 91125, 157.3),
+             (4096, 11008, 4096, "bf16", 0.331, 1000, 68318250, 2516.6),
+             (64, 4096, 4096, "bf16", 0.0146, 1000, 34780200, 2516.6),
+             (1024, 1024, 1024, "f32", 0.0285, 200, 23393656, 157.3)]
+    for M, N, K, dt, ms, timed, size, peak in cases:
+        r = gt.report(M, N, K, dt, ms, timed, size, peak)
+        t = F(2 * M * N * K) / (F(ms) / 1000) / 10 ** 12
+        close(r["tflops"], t)
+        close(r["pct_of_peak"], 100 * t / F(peak))
+        close(r["fraction_of_space_pct"], F(100 * timed, size))
+        esz = 2 if dt == "bf16" else 4
+        assert r["algorithmic_bytes"] == (M * K + K * N) * esz + M * N * 4
+        close(r["hbm_gbs"], F(r["algorithmic_bytes"]) / (F(ms) / 1000) / 10 ** 9)
+    # the workload list's budgets as shares of their spaces (exact values)
+    assert gt.report(4096, 4096, 4096, "bf16", 1.0, 1000, 188392750, 1)["fraction_of_space_pct"] \
+        == 100 * 1000 / 188392750
+    assert F(1000, 188392750) < F(1, 100)     # the search explores under 1 % of the space
+    # 1 ms at 4096³: 137.438953472 TFLOP/s exactly
+    assert gt.report(4096, 4096, 4096, "bf16", 1.0, 1, 1, 1)["tflops"] == 137.438953472

@@ -218,3 +218,22 @@ def test_legit_grid_limits(orc):
     sk = orc.Space(1, 1, 131072, (1, 4, 1), "f32", False)
     assert not sk.legit(((1,), (1, 131072, 1, 1), (1,), 0))    # kSplit 2^17 > 65535
     assert sk.legit(((1,), (4, 32768, 1, 1), (1,), 0))
+
+
+def test_legit_whole_launch(orc):
+    # the whole dispatch, grid_M * grid_N * kSplit * 64 * waves work-items,
+    # stays below 2^32
+    sp = orc.Space(4096, 4096, 4096, (4, 4, 4), "bf16", True)
+    # paper start state: 2^24 one-wave workgroups = 2^30 work-items
+    assert sp.legit(((4096, 1, 1, 1), (4096, 1, 1, 1), (4096, 1, 1, 1), 16))
+    # the same grid split two ways along K: 2^31; four ways: 2^32
+    assert sp.legit(((4096, 1, 1, 1), (2048, 2, 1, 1), (4096, 1, 1, 1), 16))
+    assert not sp.legit(((4096, 1, 1, 1), (1024, 4, 1, 1), (4096, 1, 1, 1), 16))
+    # every K element its own workgroup: 2^24 * 4096 * 64 = 2^42
+    assert not sp.legit(((4096, 1, 1, 1), (1, 4096, 1, 1), (4096, 1, 1, 1), 16))
+    # 2^19 tiles of 8 waves, split 4096 ways: 2^19 * 2^12 * 512 = 2^40
+    assert not sp.legit(((512, 2, 1, 4), (1, 4096, 1, 1), (1024, 4, 1, 1), 32))
+    # the same tiles without the split: 2^28 work-items
+    assert sp.legit(((512, 2, 1, 4), (4096, 1, 1, 1), (1024, 4, 1, 1), 32))
+    # 256 tiles of 4 waves split 64 ways: 256 * 64 * 256 = 2^22
+    assert sp.legit(((16, 2, 4, 32), (1, 64, 4, 16), (16, 2, 4, 32), 32))
