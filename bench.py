@@ -239,6 +239,10 @@ def main():
     ap.add_argument("--rho", type=int, default=5)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--mode", choices=["adjacent", "any"], default="adjacent")
+    ap.add_argument("--progress", type=float, default=0.0,
+                    help="> 0: a search progress line on stderr at most this often (s)")
+    ap.add_argument("--t-max", type=float, default=0.0,
+                    help="> 0: search time limit in seconds (T_max of Alg.1)")
     ap.add_argument("--no-enumeration", action="store_true",
                     help="skip the timed full enumeration of the space")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
@@ -322,7 +326,8 @@ def main():
     def step():
         with torch.cuda.stream(stream):
             res = gt.tune_gbfs(sp, budget=budget, s0=s0, rho=args.rho, seed=args.seed,
-                               A=Ad, B=Bd, C=C, c_ref=Cref, stream=stream)
+                               A=Ad, B=Bd, C=C, c_ref=Cref, stream=stream,
+                               progress_s=args.progress, t_max_s=args.t_max)
             # report: the TOPK configurations of the log with the lowest
             # (10-run) costs are re-timed over REPEAT launches each, s* first;
             # the fastest is the reported configuration

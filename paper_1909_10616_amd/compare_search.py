@@ -34,6 +34,8 @@ def main():
     ap.add_argument("--s0", choices=["hand", "paper"], default="hand")
     ap.add_argument("--rho", type=int, default=5)
     ap.add_argument("--out", default=None)
+    ap.add_argument("--progress", type=float, default=0.0,
+                    help="> 0: a progress line on stderr at most this often (s)")
     ap.add_argument("--trace", action="store_true",
                     help="name every candidate on stderr before it is launched")
     args = ap.parse_args()
@@ -62,7 +64,7 @@ def main():
         for name, fn in (("gbfs", gt.tune_gbfs), ("random", gt.tune_random)):
             # every candidate is named on stderr before it is launched
             kw = dict(budget=budget, seed=seed, t_max_s=args.t_max, A=Ad, B=Bd, C=C, c_ref=R,
-                      trace_fd=2 if args.trace else -1)
+                      trace_fd=2 if args.trace else -1, progress_s=args.progress)
             if name == "gbfs":
                 kw.update(s0=s0, rho=args.rho)
             print(f"seed {seed} {name}: searching", flush=True)
