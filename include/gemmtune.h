@@ -145,6 +145,18 @@ int gt_reference_gemm(const void* A, const void* B, void* C, int64_t M,
 int gt_compare(const void* C, const void* R, int64_t n, void* stream,
                double* rel);
 
+/* gt_compare for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same result, with the two result words held in a static 256-byte
+ * device array of the library (one copy per GPU, kept until the process
+ * ends) instead of the buffer gt_compare allocates on first use. No
+ * hipMalloc, hipFree or other allocating call is made; n is not limited (the
+ * kernels reduce any n into the two words). Calls that overlap on one GPU
+ * race on that array; each call clears it before use. Synchronises the
+ * stream. GT_EINVAL for null pointers or n < 1, GT_EHIP for a HIP failure. */
+int gt_compare_noalloc(const void* C, const void* R, int64_t n, void* stream,
+                       double* rel);
+
 /* How a configuration lowers (for reports and tests). */
 typedef struct gt_kernel_info {
   int32_t I, IK;             /* MFMA instruction size and its K */

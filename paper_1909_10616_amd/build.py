@@ -36,6 +36,7 @@ def _units():
         ("search", "search.cpp", []),
         ("runtime", "runtime.cpp", []),
         ("aux_kernels", "aux_kernels.hip", []),
+        ("noalloc", "noalloc.hip", []),
     ]
     units.append(("gemm_lookup", "gemm_lookup.cpp", []))
     for dt, dn in ((0, "f32"), (1, "bf16")):

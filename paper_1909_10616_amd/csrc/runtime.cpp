@@ -152,6 +152,28 @@ std::mutex g_cmp_mu;
 unsigned* g_cmp_buf[64] = {};  // per device, 2 words, kept until process exit
 }  // namespace
 
+int compare_into(const void* C, const void* R, int64_t n, unsigned* buf, hipStream_t s,
+                 double* rel) {
+  hipError_t e =
+      launch_compare(static_cast<const float*>(C), static_cast<const float*>(R), n, buf, s);
+  if (e != hipSuccess) return hip_fail(e, "compare launch");
+  unsigned host[2];
+  e = hipMemcpyAsync(host, buf, sizeof(host), hipMemcpyDeviceToHost, s);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (compare result)");
+  e = hipStreamSynchronize(s);
+  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize (compare)");
+  float md, mr;
+  std::memcpy(&md, &host[0], 4);
+  std::memcpy(&mr, &host[1], 4);
+  if (std::isnan(md))
+    *rel = NAN;
+  else if (mr == 0.0f)
+    *rel = md == 0.0f ? 0.0 : INFINITY;
+  else
+    *rel = static_cast<double>(md) / static_cast<double>(mr);
+  return GT_OK;
+}
+
 int compare_on_gpu(const void* C, const void* R, int64_t n, hipStream_t s, double* rel) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
@@ -169,23 +191,7 @@ int compare_on_gpu(const void* C, const void* R, int64_t n, hipStream_t s, doubl
     }
     buf = g_cmp_buf[dev];
   }
-  e = launch_compare(static_cast<const float*>(C), static_cast<const float*>(R), n, buf, s);
-  if (e != hipSuccess) return hip_fail(e, "compare launch");
-  unsigned host[2];
-  e = hipMemcpyAsync(host, buf, sizeof(host), hipMemcpyDeviceToHost, s);
-  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (compare result)");
-  e = hipStreamSynchronize(s);
-  if (e != hipSuccess) return hip_fail(e, "hipStreamSynchronize (compare)");
-  float md, mr;
-  std::memcpy(&md, &host[0], 4);
-  std::memcpy(&mr, &host[1], 4);
-  if (std::isnan(md))
-    *rel = NAN;
-  else if (mr == 0.0f)
-    *rel = md == 0.0f ? 0.0 : INFINITY;
-  else
-    *rel = static_cast<double>(md) / static_cast<double>(mr);
-  return GT_OK;
+  return compare_into(C, R, n, buf, s, rel);
 }
 
 int measure(const gt_config& c, const void* A, const void* B, void* C, int64_t M, int64_t N,

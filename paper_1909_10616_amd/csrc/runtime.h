@@ -29,5 +29,9 @@ int measure(const gt_config& c, const void* A, const void* B, void* C, int64_t M
             int64_t K, int dtype, hipStream_t s, int warmup, int runs, double abort_ms,
             double* mean_ms, double* first_ms, int* aborted, RunStats* stats);
 int compare_on_gpu(const void* C, const void* R, int64_t n, hipStream_t s, double* rel);
+// The comparison with a caller-chosen 2-word device buffer (cleared by a
+// kernel, filled by the reduction, read back; synchronises the stream).
+int compare_into(const void* C, const void* R, int64_t n, unsigned* buf, hipStream_t s,
+                 double* rel);
 
 }  // namespace gt

@@ -95,7 +95,7 @@ class gt_tune_result(ctypes.Structure):
 EXPORTS = ("gt_space_size", "enumerate_configs", "config_rank", "config_unrank", "config_legit",
            "neighbours", "gemm_run", "gt_measure", "gt_reference_gemm", "gt_compare",
            "gt_lower", "gt_tune_opts_init", "tune_gbfs", "tune_random", "gt_na2c_params_init",
-           "tune_na2c", "gt_shutdown", "gt_last_error")
+           "tune_na2c", "gt_shutdown", "gt_compare_noalloc", "gt_last_error")
 
 _lib = None
 
@@ -133,6 +133,7 @@ def lib():
     L.tune_na2c.argtypes = [SP, ctypes.POINTER(gt_tune_opts), ctypes.POINTER(gt_na2c_params),
                             gt_cost_fn, P, ctypes.POINTER(gt_tune_result)]
     L.gt_shutdown.argtypes = []
+    L.gt_compare_noalloc.argtypes = [P, P, i64, P, ctypes.POINTER(ctypes.c_double)]
     L.gt_last_error.restype = ctypes.c_char_p
     for name in EXPORTS:
         if name != "gt_last_error":
@@ -299,6 +300,16 @@ def gt_reference_gemm(A, B, C, stream=None, a_kmajor=False):
     _check(lib().gt_reference_gemm(A.data_ptr(), B.data_ptr(), C.data_ptr(), M, N, K, dt,
                                    _stream(stream)), "gt_reference_gemm")
     return C
+
+
+def gt_compare_noalloc(C, R, stream=None) -> float:
+    """gt_compare without any device allocation (the result words live in a
+    static device array of the library)."""
+    assert C.numel() == R.numel() and C.is_cuda and R.is_cuda
+    rel = ctypes.c_double()
+    _check(lib().gt_compare_noalloc(C.data_ptr(), R.data_ptr(), C.numel(), _stream(stream),
+                                    ctypes.byref(rel)), "gt_compare_noalloc")
+    return rel.value
 
 
 def gt_shutdown():
