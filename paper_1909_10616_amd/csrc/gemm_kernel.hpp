@@ -651,7 +651,13 @@ __device__ void gemm_fast(const KArgs& a, char* smem) {
 // LDS slots (lane j → slot base + j) from 64 per-lane global addresses, so
 // tiles reach LDS without passing through registers and a ring of ns stages
 // keeps ns − 1 stages of loads in flight. A sits in LDS as [m][k] chunks,
-// XOR-swizzled by swz(); B stays [k][n] with the chunks of row k XOR-ed by
+// XOR-swizzled by swz(); with 16×16 MFMA and stages of two or more
+// chunk-steps (64- and 128-deep) it is split into planes instead, one per
+// chunk-step: plane cs holds the G = 4 chunks that step reads of every one of
+// the BM rows, as [m][4] swizzled by swz(). Each fragment read then covers
+// one aligned 1 KiB block, which the 16-byte LDS reads serve without bank
+// conflicts; the stage-wide layout conflicts 2-way at those depths (with
+// 32×32 MFMA, or 32-deep stages, it does not, and is kept). B stays [k][n] with the chunks of row k XOR-ed by
 // bswz(k), and its MFMA operands are read with the transposing LDS read: inside a
 // 16-lane group, lane l receives element (l & 3) of the 8 bytes addressed by
 // lane 4j + (l >> 2) as its j-th value, so lanes addressing rows k0 + (i >> 2),
@@ -784,9 +790,12 @@ __device__ __forceinline__ void gemm_fast_dl(const KArgs& a, char* smem) {
   // Load instruction p of a stage fills slots p·64 … p·64+63; wavefront w
   // issues p = w, w + nw, … (A instructions first, then B). Each lane works
   // out the chunk its slot holds: A slot s holds chunk swz(s) (swz is an
-  // involution), B slot (k, cs) holds row k, chunk cs ^ bswz(k). The lane's
-  // byte offset from the stage's A (or B) origin is the same for every stage,
-  // so it is computed once (it fits 32 bits: BM·K and BK·N are below 2^31).
+  // involution) of the [m][k] layout, or in the plane layout chunk-step
+  // s / (4·BM) and in-plane chunk swz(s mod 4·BM) of its [m][4]; B slot
+  // (k, cs) holds row k, chunk cs ^ bswz(k). The lane's byte offset from the
+  // stage's A (or B) origin is the same for every stage, so it is computed
+  // once (it fits 32 bits: BM·K and BK·N are below 2^31).
+  constexpr bool PLANES = I == 16 && NCS >= 2;
   const int lgcprb = a.lgBN - 3;
   const int na_w = pa / nw;
   uint32_t doff[kMaxDlInst];
@@ -794,9 +803,17 @@ __device__ __forceinline__ void gemm_fast_dl(const KArgs& a, char* smem) {
   for (int i = 0; i < kMaxDlInst; ++i) {
     doff[i] = 0;
     if (i < na_w) {
-      const int q = swz(((wave + i * nw) << 6) + lane);
-      doff[i] = (static_cast<uint32_t>(q >> LGCPR) * static_cast<uint32_t>(a.K) +
-                 static_cast<uint32_t>((q & (CPR - 1)) << 3)) * 2u;
+      if constexpr (PLANES) {
+        const int s = ((wave + i * nw) << 6) + lane;
+        const int lgp = a.lgBM + 2;  // slots per plane: BM·4
+        const int q = swz(s & ((1 << lgp) - 1));
+        doff[i] = (static_cast<uint32_t>(q >> 2) * static_cast<uint32_t>(a.K) +
+                   static_cast<uint32_t>((((s >> lgp) << 2) + (q & 3)) << 3)) * 2u;
+      } else {
+        const int q = swz(((wave + i * nw) << 6) + lane);
+        doff[i] = (static_cast<uint32_t>(q >> LGCPR) * static_cast<uint32_t>(a.K) +
+                   static_cast<uint32_t>((q & (CPR - 1)) << 3)) * 2u;
+      }
     } else if (i < ninst) {
       const int sidx = ((wave + (i - na_w) * nw) << 6) + lane;
       const int k = sidx >> lgcprb, cs = sidx & (cprb - 1);
@@ -846,16 +863,22 @@ __device__ __forceinline__ void gemm_fast_dl(const KArgs& a, char* smem) {
 #pragma unroll
     for (int j = 0; j < TN; ++j) acc[i][j] = acc_t{};
 
-  // A fragment slots as in the register-staged path.
+  // A fragment slots: in the [m][k] layout as in the register-staged path;
+  // in the plane layout, this lane's slot in plane 0 (plane cs adds 4·BM·cs).
   const int grp = lane / I;
   int xa[TM][NLINE];
 #pragma unroll
   for (int t = 0; t < TM; ++t)
 #pragma unroll
     for (int j = 0; j < NLINE; ++j) {
-      const int q0 = ((wm * a.WM + t * I + (lane % I)) << LGCPR) + grp + 8 * j;
-      xa[t][j] = swz(q0) - 8 * j;
+      if constexpr (PLANES) {
+        xa[t][j] = swz(((wm * a.WM + t * I + (lane % I)) << 2) + grp);
+      } else {
+        const int q0 = ((wm * a.WM + t * I + (lane % I)) << LGCPR) + grp + 8 * j;
+        xa[t][j] = swz(q0) - 8 * j;
+      }
     }
+  const int plane_slots = BM << 2;
   // B operand addressing: in 16-lane group g16, input lane i covers row
   // k0 + (i >> 2) (+4 for the second read), columns n0 + 4(i & 3).
   const int i16 = lane & 15, g16 = lane >> 4;
@@ -872,7 +895,12 @@ __device__ __forceinline__ void gemm_fast_dl(const KArgs& a, char* smem) {
     const int c = cs * G;
     const int j = CPR >= 8 ? (c >> 3) : 0;
 #pragma unroll
-    for (int t = 0; t < TM; ++t) fa[fs][t] = as[(xa[t][j] ^ (c & 7)) + (c & ~7)];
+    for (int t = 0; t < TM; ++t) {
+      if constexpr (PLANES)
+        fa[fs][t] = as[cs * plane_slots + xa[t][0]];
+      else
+        fa[fs][t] = as[(xa[t][j] ^ (c & 7)) + (c & ~7)];
+    }
     const char* bs = reinterpret_cast<const char*>(as + achunks);
 #pragma unroll
     for (int t = 0; t < TN; ++t) {

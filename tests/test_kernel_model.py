@@ -55,6 +55,34 @@ def bswz(k, cprb):
     return (((j << 2) | (((j ^ (j >> 1)) & 1) << 1)) ^ (((k >> 3) & 1) << 3)) & (cprb - 1)
 
 
+def a_planes(I, CPR):
+    """The plane layout: 16×16 MFMA and stages of two or more chunk-steps."""
+    return I == 16 and CPR // 4 >= 2
+
+
+def a_slot_chunk(s, I, BM, CPR):
+    """(row, chunk) of the A tile that direct-load slot s of a stage holds:
+    the plane layout (plane s // 4BM, [m][4] swizzled) or the stage-wide
+    [m][k] layout."""
+    if a_planes(I, CPR):
+        lgp = lg(BM) + 2
+        q = swz(s & ((1 << lgp) - 1))
+        return q >> 2, ((s >> lgp) << 2) + (q & 3)
+    q = swz(s)
+    return q >> lg(CPR), q & (CPR - 1)
+
+
+def a_read_slot(I, BM, CPR, row, grp, cs):
+    """LDS slot a lane reads for A row `row`, chunk cs·G + grp."""
+    G = 64 // I
+    if a_planes(I, CPR):
+        return cs * (BM << 2) + swz((row << 2) + grp)
+    c = cs * G
+    j = (c >> 3) if CPR >= 8 else 0
+    xa = swz((row << lg(CPR)) + grp + 8 * j) - 8 * j
+    return (xa ^ (c & 7)) + (c & ~7)
+
+
 def lg(v):
     r = v.bit_length() - 1
     assert 1 << r == v
@@ -103,10 +131,10 @@ def frag_steps(L, CPR, lane):
             yield w, wm, wn, c, j, LGCPR, grp
 
 
-def check_c_and_frags(L, CPR, achunks, lane, bt_rows=None):
+def check_c_and_frags(L, CPR, achunks, lane, bt_rows=None, a_slots=True):
     I = L["I"]
     for w, wm, wn, c, j, LGCPR, grp in frag_steps(L, CPR, lane):
-        for t in range(L["TM"]):
+        for t in range(L["TM"] if a_slots else 0):
             q0 = ((wm * L["WM"] + t * I + lane % I) << LGCPR) + grp + 8 * j
             idx = ((swz(q0) - 8 * j) ^ (c & 7)) + (c & ~7)
             assert idx.min() >= 0 and idx.max() < achunks
@@ -199,11 +227,18 @@ def check_dl(L, info, M, N, K):
     assert ninst <= cap and 2 <= ns <= 8
     assert ns * stage * 16 <= info["lds_bytes"] <= LDS_MAX
     lane = np.arange(64)
+    # which chunk each A slot holds: every chunk of the stage exactly once
+    slots = np.arange(achunks)
+    arow, achk = a_slot_chunk(slots, I, BM, CPR)
+    assert arow.max() < BM and achk.max() < CPR
+    assert len(np.unique(arow * CPR + achk)) == achunks
+    held = np.empty(achunks, dtype=np.int64)
+    held[slots] = arow * CPR + achk
     for w in range(W):
         for i in range(ninst):
             if i < na_w:
-                q = swz(((w + i * W) << 6) + lane)
-                off = ((q >> LGCPR) * K + ((q & (CPR - 1)) << 3)) * 2
+                row, chunk = a_slot_chunk(((w + i * W) << 6) + lane, I, BM, CPR)
+                off = (row * K + (chunk << 3)) * 2
                 dst = (w + i * W) * 1024
                 lim = M * K * 2
             else:
@@ -223,17 +258,28 @@ def check_dl(L, info, M, N, K):
     i16, g16 = lane & 15, lane >> 4
     kgrp = (g16 >> 1) if I == 32 else g16
     ncol0 = (16 * (g16 & 1) if I == 32 else 0) + 4 * (i16 & 3)
+    krow_l = kgrp * 8 + (i16 >> 2)
     for w in range(W):
-        wn = w // L["wavesM"]
+        wm, wn = w % L["wavesM"], w // L["wavesM"]
         for cs in range(NCS):
             for t in range(TN):
                 col = wn * L["WN"] + t * I + ncol0
                 for hh in range(2):
-                    k = cs * G * 8 + kgrp * 8 + (i16 >> 2) + 4 * hh
+                    k = cs * G * 8 + krow_l + 4 * hh
                     assert k.max() < BK and col.max() < BN
-                    addr = (k * cprb + ((col >> 3) ^ bswz(k, cprb))) * 16 + (col & 4) * 2
+                    bx = np.array([bswz(int(x), cprb) for x in k])
+                    chunk = (col >> 3) ^ bx
+                    addr = (k * cprb + chunk) * 16 + (col & 4) * 2
                     assert addr.min() >= 0 and addr.max() + 8 <= bchunks * 16
-    check_c_and_frags(L, CPR, achunks, lane)
+                    # slot (k, chunk) holds column chunk chunk ^ bswz(k) of row k
+                    assert np.array_equal(chunk ^ bx, col >> 3)
+            # A: the slot each lane reads holds its row and chunk
+            for t in range(L["TM"]):
+                row = wm * L["WM"] + t * I + lane % I
+                slot = a_read_slot(I, BM, CPR, row, lane // I, cs)
+                assert slot.min() >= 0 and slot.max() < achunks
+                assert np.array_equal(held[slot], row * CPR + cs * G + lane // I)
+    check_c_and_frags(L, CPR, achunks, lane, a_slots=False)
     ring_schedule(TM * TN, NCS, cap, ninst, ns, L["kLoop"])
 
 
