@@ -162,6 +162,8 @@ FULL = [
     ("gemm4096_bf16", ((16, 2, 8, 16), (128, 1, 1, 32), (16, 4, 1, 64), 16)),
     ("mlp4096x11008x4096_bf16", ((16, 2, 4, 32), (64, 1, 4, 16), (43, 2, 4, 32), 32)),
     ("skinny64x4096x4096_bf16", ((1, 1, 2, 32), (16, 8, 2, 16), (32, 2, 2, 32), 32)),
+    # 64x64 tiles, four K slices (8 wavefronts, direct-load ring)
+    ("skinny64x4096x4096_bf16", ((1, 2, 2, 16), (8, 4, 1, 128), (64, 4, 1, 16), 16)),
     ("gemm1024_f32", ((8, 2, 2, 32), (32, 1, 4, 8), (8, 2, 2, 32), 0)),
     ("gemm2048_f32", ((16, 2, 2, 32), (64, 1, 4, 8), (16, 2, 2, 32), 0)),
 ]
@@ -212,10 +214,37 @@ def test_split_k_smallint_bit_exact(gt, orc):
     ref = orc.gemm(raw_bytes(A), raw_bytes(B), M, N, K, "bf16")
     for cfg in [((1, 1, 2, 32), (4, 8, 2, 16), (4, 2, 1, 32), 32),
                 ((2, 2, 1, 16), (2, 64, 1, 8), (2, 2, 2, 32), 16),
-                ((64, 1, 1, 1), (1, 1024, 1, 1), (256, 1, 1, 1), 16)]:
+                ((64, 1, 1, 1), (1, 1024, 1, 1), (256, 1, 1, 1), 16),
+                # 256 accumulators per lane (AGPRs)
+                ((1, 1, 2, 32), (8, 4, 2, 16), (1, 1, 8, 32), 32)]:
         note(f"split-K {cfg} {gt.lower(cfg, M, N, K, 'bf16')}")
         C = run(gt, cfg, A, B)
         assert np.array_equal(C.astype(np.float64), ref), cfg
+
+
+SPLITK_PATHS = [
+    # (dtype, configuration, (fast, dl)) at 64x256x1024, split K
+    ("bf16", ((2, 1, 2, 16), (16, 4, 4, 4), (2, 2, 2, 32), 16), (0, 0)),   # generic
+    ("f32", ((2, 1, 2, 16), (16, 4, 4, 4), (2, 2, 2, 32), 16), (1, 0)),    # register-staged
+    ("f32", ((2, 2, 1, 16), (4, 4, 8, 8), (4, 2, 2, 16), 0), (1, 0)),
+    ("bf16", ((1, 1, 2, 32), (4, 8, 2, 16), (4, 2, 1, 32), 32), (1, 1)),   # direct-load
+    ("bf16", ((1, 1, 2, 32), (8, 4, 4, 8), (4, 1, 2, 32), 32), (0, 0)),
+]
+
+
+@pytest.mark.parametrize("case", SPLITK_PATHS, ids=[f"{c[0]}-{i}" for i, c in enumerate(SPLITK_PATHS)])
+def test_split_k_every_path_bit_exact(gt, orc, case):
+    """Split K on each kernel path (the clear of C, then fp32 atomics from
+    every slice), exact on small integers in any order of the adds."""
+    dt, cfg, path = case
+    M, N, K = 64, 256, 1024
+    info = gt.lower(cfg, M, N, K, dt)
+    note(f"split-K {dt} {cfg} {info}")
+    assert (info["fast"], info["dl"]) == path and info["grid_y"] > 1
+    A, B = make_inputs(M, N, K, dt, 9, "smallint")
+    ref = orc.gemm(raw_bytes(A), raw_bytes(B), M, N, K, dt)
+    C = run(gt, cfg, A, B)
+    assert np.array_equal(C.astype(np.float64), ref), cfg
 
 
 def test_reference_compare_and_measure(gt, orc):
