@@ -13,9 +13,9 @@
       a plain device copy of that size).
   python -m paper_1909_10616_amd.profsum bestcfg BENCH_JSON
       the best configuration of a bench line, as the JSON bench.py --replay takes.
-  python -m paper_1909_10616_amd.profsum report OUT
-      markdown summary of a profile_bench.sh output folder, ending with the
-      line for profiles/traffic.txt.
+  python -m paper_1909_10616_amd.profsum report OUT [--args "EXTRA BENCH ARGUMENTS"]
+      markdown summary of a profile_bench.sh output folder (run with those
+      extra bench.py arguments), ending with the line for profiles/traffic.txt.
 """
 from __future__ import annotations
 
@@ -118,7 +118,7 @@ def _last_line_json(path):
     return json.loads(lines[-1])
 
 
-def report(out, copy_bytes=1 << 30):
+def report(out, copy_bytes=1 << 30, extra=""):
     b = _last_line_json(os.path.join(out, "bench_traced.json"))
     c = b["config"]
     kname = c["kernel_name"]
@@ -142,14 +142,15 @@ def report(out, copy_bytes=1 << 30):
     L.append("")
     L.append("Commands (from the repository root on the GPU host; OUT is the output folder):")
     L.append("")
-    L.append("    paper_1909_10616_amd/profile_bench.sh OUT")
+    x = (" " + extra) if extra else ""
+    L.append(f"    paper_1909_10616_amd/profile_bench.sh OUT{x}")
     L.append("      = rocprofv3 --kernel-trace --stats --output-format csv -d OUT/trace -o bench -- "
-             "python3 bench.py --no-cpu-baseline")
-    L.append("        rocprofv3 --pmc FETCH_SIZE   (then WRITE_SIZE) ... -- python3 bench.py --replay CFG --repeat 20")
+             f"python3 bench.py --no-cpu-baseline{x}")
+    L.append(f"        rocprofv3 --pmc FETCH_SIZE   (then WRITE_SIZE) ... -- python3 bench.py{x} --replay CFG --repeat 20")
     L.append("        rocprofv3 --pmc FETCH_SIZE   (then WRITE_SIZE) ... -- python3 bench.py --calibrate-copy 1024 --repeat 5")
     L.append("        rocprofv3 --pmc SQ_VALU_MFMA_BUSY_CYCLES GRBM_GUI_ACTIVE SQ_LDS_BANK_CONFLICT "
-             "SQ_LDS_IDX_ACTIVE SQ_WAVE_CYCLES SQ_WAIT_ANY ... -- python3 bench.py --replay CFG --repeat 20")
-    L.append("    python3 paper_1909_10616_amd/profsum.py report OUT")
+             f"SQ_LDS_IDX_ACTIVE SQ_WAVE_CYCLES SQ_WAIT_ANY ... -- python3 bench.py{x} --replay CFG --repeat 20")
+    L.append("    python3 paper_1909_10616_amd/profsum.py report OUT" + (f' --args "{extra}"' if extra else ""))
     L.append("")
     L.append(f"Best configuration of the traced search: `{c['best_config']}` (CFG), "
              f"{c['configs_timed']} configurations timed of {c['space_size']} "
@@ -211,11 +212,12 @@ def main():
     ap.add_argument("--last", type=int, default=0)
     ap.add_argument("--copy-bytes", type=float, default=0)
     ap.add_argument("--copy-kernel", default="copy")
+    ap.add_argument("--args", default="", help="report: the extra bench.py arguments of the profile")
     a = ap.parse_args()
     if a.mode == "bestcfg":
         print(json.dumps(best_cfg(a.dirs[0])))
     elif a.mode == "report":
-        print(report(a.dirs[0]))
+        print(report(a.dirs[0], extra=a.args))
     elif a.mode == "trace":
         print(trace(a.dirs[0], a.dirs[1], a.kernel, a.grid, a.lds, a.last))
     elif a.mode == "pmc":
