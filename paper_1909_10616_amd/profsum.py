@@ -107,7 +107,7 @@ def traffic(fetch_dir, write_dir, cfetch_dir, cwrite_dir, copy_bytes, kernel, gr
 
 
 def best_cfg(bench_json):
-    d = json.load(open(bench_json))
+    d = _last_line_json(bench_json)
     m = re.match(r"m(\[.*?\])k(\[.*?\])n(\[.*?\])mfma(\d+)", d["config"]["best_config"])
     return [json.loads(m.group(1)), json.loads(m.group(2)), json.loads(m.group(3)), int(m.group(4))]
 
