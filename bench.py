@@ -110,8 +110,8 @@ def host_info():
 
 def cpu_threads():
     """Threads for the oracle: the CPU share the job is given (OMP_NUM_THREADS
-    when set, which the GPU machine sets to its per-GPU share), else every CPU
-    this process may use."""
+    when set, as a scheduler does for each GPU's share of the host), else
+    every CPU this process may use."""
     aff = len(os.sched_getaffinity(0))
     return max(1, min(int(os.environ.get("OMP_NUM_THREADS", "0")) or aff, aff))
 
