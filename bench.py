@@ -95,6 +95,52 @@ def measured_traffic(w, info):
     return None
 
 
+def roofline(dtype, M, N, K, alg_bytes, tflops, hbm_gbs, traffic):
+    """The bench line's roofline: the bound is the one the workload's
+    arithmetic intensity (2MNK / algorithmic bytes) puts it under — MFMA at
+    or above the ridge (the dtype's MFMA peak over the HBM bandwidth), HBM
+    below it; the other unit's fraction is given beside it."""
+    flops = 2.0 * M * N * K
+    peak = PEAK[dtype]
+    ridge = peak * 1e12 / (HBM_GBS * 1e9)
+    if flops / alg_bytes >= ridge:
+        r = {"bound": "mfma", "achieved": round(tflops, 2), "peak": peak, "unit": "TFLOP/s",
+             "frac": round(tflops / peak, 4)}
+        other = {"hbm_gbs_at_algorithmic_bytes": round(hbm_gbs, 1),
+                 "hbm_frac": round(hbm_gbs / HBM_GBS, 4)}
+    else:
+        r = {"bound": "hbm", "achieved": round(hbm_gbs, 1), "peak": HBM_GBS, "unit": "GB/s",
+             "frac": round(hbm_gbs / HBM_GBS, 4)}
+        other = {"mfma_tflops": round(tflops, 2), "mfma_frac": round(tflops / peak, 4)}
+    r.update({"traffic": traffic, "algorithmic_bytes": alg_bytes,
+              "arithmetic_intensity": round(flops / alg_bytes, 1), "ridge": round(ridge, 1)})
+    r.update(other)
+    return r
+
+
+def flushed_timing(run, stream, mib, runs=50):
+    """Median time of `run` with a `mib` MiB buffer read on the stream before
+    each launch (more than the 256 MiB last-level cache, so A and B come from
+    HBM; the buffer is written once beforehand, so the lines it leaves in the
+    cache are clean and evicting them costs no write-back), each launch
+    between its own pair of events."""
+    import torch
+    buf = torch.ones(mib << 18, dtype=torch.float32, device="cuda:0")
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(runs)]
+    with torch.cuda.stream(stream):
+        for e0, e1 in evs:
+            buf.sum()
+            e0.record(stream)
+            run()
+            e1.record(stream)
+    torch.cuda.synchronize()
+    d = sorted(e0.elapsed_time(e1) for e0, e1 in evs)
+    del buf
+    return d[runs // 2] if runs % 2 else 0.5 * (d[runs // 2 - 1] + d[runs // 2])
+
+
 def host_info():
     """The host the CPU baseline runs on: logical CPUs, the CPUs this process
     may use, and the CPU model."""
@@ -246,6 +292,9 @@ def main():
     ap.add_argument("--no-enumeration", action="store_true",
                     help="skip the timed full enumeration of the space")
     ap.add_argument("--cpu-seconds", type=float, default=20.0)
+    ap.add_argument("--flush-mib", type=int, default=0,
+                    help="> 0: also time the reported configuration with this many MiB read "
+                         "before each launch (larger than the 256 MiB last-level cache)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--log-out", default=None, help="write the search log (JSON) here")
     ap.add_argument("--replay", default=None,
@@ -428,13 +477,17 @@ def main():
             "kernel_name": kernel_name(w, info), "launch_signature": launch_signature(w, info),
             "kernel_source": kernel_source_hash(),
         },
-        "roofline": {
-            "bound": "mfma", "achieved": round(value, 2), "peak": peak, "unit": "TFLOP/s",
-            "frac": round(value / peak, 4), "traffic": measured_traffic(w, info),
-            "algorithmic_bytes": alg_bytes,
-            "hbm_gbs_at_algorithmic_bytes": round(fig["hbm_gbs"], 1),
-        },
+        "roofline": roofline(w.dtype, w.M, w.N, w.K, alg_bytes, value, fig["hbm_gbs"],
+                             measured_traffic(w, info)),
     }
+    if args.flush_mib > 0:
+        log(f"timing with {args.flush_mib} MiB read before each launch ...")
+        fl_ms = flushed_timing(lambda: gt.gemm_run(last["best"], Ad, Bd, C, stream=stream), stream,
+                               args.flush_mib)
+        out["config"]["flushed"] = {
+            "flush_mib": args.flush_mib, "flush": "read", "runs": 50, "median_ms": fl_ms,
+            "tflops": round(gt.tflops(w.M, w.N, w.K, fl_ms), 2),
+            "hbm_gbs_at_algorithmic_bytes": round(alg_bytes / (fl_ms * 1e-3) / 1e9, 1)}
     out["device"] = device_info()
     if not args.no_enumeration:
         log("library enumeration of the space ...")

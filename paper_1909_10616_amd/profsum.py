@@ -175,7 +175,10 @@ def report(out, copy_bytes=1 << 30, extra=""):
              f"{b['config']['best_ms'] * 1e3:.2f} | {b['value']:.1f} |")
     L.append(f"| median of the traced dispatches | | {statistics.median(dur):.2f} | |")
     L.append("")
-    L.append(f"Fraction of MFMA peak ({b['roofline']['peak']} TFLOP/s): {b['roofline']['frac']:.4f}.")
+    rf = b["roofline"]
+    L.append(f"Roofline ({rf.get('bound', 'mfma')} bound): {rf.get('achieved')} {rf.get('unit', 'TFLOP/s')} "
+             f"of {rf['peak']} {rf.get('unit', 'TFLOP/s')}, fraction {rf['frac']:.4f}"
+             + (f"; MFMA fraction {rf['mfma_frac']:.4f}" if "mfma_frac" in rf else "") + ".")
     L.append("")
     L.append("## HBM traffic per launch (FETCH_SIZE, WRITE_SIZE; scaled by a 1 GiB copy)")
     L.append("")

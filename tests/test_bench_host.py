@@ -61,3 +61,24 @@ def test_committed_traffic_line_matches_the_sources(bench):
     lines = [l for l in open(os.path.join(ROOT, "profiles", "traffic.txt"))
              if not l.startswith("#") and "|" in l]
     assert any(f"source={bench.kernel_source_hash()}" in l for l in lines)
+
+
+def test_roofline_bound_follows_arithmetic_intensity(bench):
+    """MFMA-bound at or above the ridge (peak over 8 TB/s), HBM-bound below
+    it, with the other unit's fraction beside it."""
+    # 4096³ bf16: 2·4096³ flop over 134,217,728 B = 1024 flop/B, ridge 314.6
+    r = bench.roofline("bf16", 4096, 4096, 4096, 134217728, 1238.36, 1209.3, 269026764)
+    assert (r["bound"], r["unit"], r["peak"], r["achieved"]) == ("mfma", "TFLOP/s", 2516.6, 1238.36)
+    assert r["frac"] == round(1238.36 / 2516.6, 4) and r["hbm_frac"] == round(1209.3 / 8000, 4)
+    assert (r["arithmetic_intensity"], r["ridge"], r["traffic"]) == (1024.0, 314.6, 269026764)
+    # 64×4096×4096 bf16: (64·4096 + 4096²)·2 + 64·4096·4 = 35,127,296 B, 61.1 flop/B
+    alg = (64 * 4096 + 4096 * 4096) * 2 + 64 * 4096 * 4
+    ms = 0.0142
+    tf, gbs = 2 * 64 * 4096 * 4096 / (ms * 1e-3) / 1e12, alg / (ms * 1e-3) / 1e9
+    r = bench.roofline("bf16", 64, 4096, 4096, alg, tf, gbs, None)
+    assert (r["bound"], r["unit"], r["peak"]) == ("hbm", "GB/s", 8000.0)
+    assert r["achieved"] == round(gbs, 1) and r["frac"] == round(gbs / 8000, 4)
+    assert r["mfma_frac"] == round(tf / 2516.6, 4) and r["arithmetic_intensity"] == 61.1
+    # 2048³ fp32: 341.3 flop/B against a ridge of 19.7
+    r = bench.roofline("f32", 2048, 2048, 2048, 3 * 2048 * 2048 * 4, 110.0, 500.0, None)
+    assert r["bound"] == "mfma" and r["ridge"] == 19.7 and r["arithmetic_intensity"] == 341.3
