@@ -82,3 +82,26 @@ def test_roofline_bound_follows_arithmetic_intensity(bench):
     # 2048³ fp32: 341.3 flop/B against a ridge of 19.7
     r = bench.roofline("f32", 2048, 2048, 2048, 3 * 2048 * 2048 * 4, 110.0, 500.0, None)
     assert r["bound"] == "mfma" and r["ridge"] == 19.7 and r["arithmetic_intensity"] == 341.3
+
+
+def test_hand_start_is_legitimate_on_every_workload(bench):
+    """The hand-crafted start: 128×128 workgroup tiles (2×2 wavefronts of
+    2×2 32-wide blocks) where 128 divides M and N, else 64×64 (one block per
+    wavefront); 32-deep K stages; legitimate in every workload's space."""
+    from paper_1909_10616_amd import gemmtune as gt
+    from workloads import WORKLOADS
+    for w in WORKLOADS.values():
+        s0 = bench.hand_s0(w)
+        sp = gt.Space(w.M, w.N, w.K, w.d, w.dtype, w.mfma_coord)
+        assert sp.legit(s0), (w.name, s0)
+        m, k, n, mfma = s0
+        assert mfma == (32 if w.mfma_coord else 0)
+        if tuple(w.d) == (4, 4, 4):
+            tile = 128 if w.M % 128 == 0 and w.N % 128 == 0 else 64
+            assert m[1:] == ((2, 2, 32) if tile == 128 else (2, 1, 32)) or w.M < 64
+            assert n[1:] == ((2, 2, 32) if tile == 128 else (2, 1, 32))
+            assert m[0] * tile == w.M and n[0] * tile == w.N and k == (w.K // 32, 1, 2, 16)
+    assert bench.hand_s0(WORKLOADS["gemm4096_bf16"]) == \
+        ((32, 2, 2, 32), (128, 1, 2, 16), (32, 2, 2, 32), 32)
+    assert bench.hand_s0(WORKLOADS["skinny64x4096x4096_bf16"]) == \
+        ((1, 2, 1, 32), (128, 1, 2, 16), (64, 2, 1, 32), 32)
