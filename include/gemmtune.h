@@ -118,10 +118,14 @@ int neighbours(const gt_space* sp, const gt_config* s, gt_config* out, int cap,
 
 /* C = A·B on the GPU with the kernel the configuration lowers to (§3.2, the
  * operator being tuned). A: M×K row-major (K×M with GT_A_KMAJOR in dtype),
- * B: K×N row-major (dtype), C: M×N row-major fp32, all device pointers. stream: hipStream_t (NULL = default).
- * Asynchronous; C is overwritten. The configuration's products must equal
- * M, K, N and it must be legitimate in the space (M, N, K, cfg->d_*, dtype,
- * mfma_coord = cfg->mfma != 0). */
+ * B: K×N row-major (dtype), C: M×N row-major fp32, all device pointers.
+ * stream: hipStream_t (NULL = default). Asynchronous; C is overwritten. The
+ * configuration's products must equal M, K, N and it must be legitimate in
+ * the space (M, N, K, cfg->d_*, dtype, mfma_coord = cfg->mfma != 0). With a
+ * K split (the second K level above 1) two kernels go on the stream: one
+ * clears C, then every slice adds its partial product with fp32 atomics, so
+ * the order of those adds, and the last bits of C, can differ from launch to
+ * launch (results on exactly representable inputs do not). */
 int gemm_run(const gt_config* cfg, const void* A, const void* B, void* C,
              int64_t M, int64_t N, int64_t K, int dtype, void* stream);
 
