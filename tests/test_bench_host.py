@@ -105,3 +105,22 @@ def test_hand_start_is_legitimate_on_every_workload(bench):
         ((32, 2, 2, 32), (128, 1, 2, 16), (32, 2, 2, 32), 32)
     assert bench.hand_s0(WORKLOADS["skinny64x4096x4096_bf16"]) == \
         ((1, 2, 1, 32), (128, 1, 2, 16), (64, 2, 1, 32), 32)
+
+
+def test_componentwise_error(bench):
+    """max |C − C*| / (|A|·|B|): rounding the oracle's fp64 product to fp32
+    stays within 2^-24 (|fl(c) − c| ≤ 2^-24·|c| ≤ 2^-24·(|A|·|B|)); an error
+    planted in one element is seen at its own scale."""
+    import numpy as np
+    import oracle
+    from workloads import make_inputs, raw_bytes
+
+    class W:
+        M, N, K, dtype = 48, 40, 64, "bf16"
+    A, B = make_inputs(W.M, W.N, W.K, W.dtype, 5, "normal")
+    C = oracle.gemm(raw_bytes(A), raw_bytes(B), W.M, W.N, W.K, W.dtype)
+    assert bench.componentwise_error(W, A, B, C.astype(np.float32), C) <= 2.0 ** -24
+    absab = np.abs(A.float().numpy().astype(np.float64)) @ np.abs(B.float().numpy().astype(np.float64))
+    Cg = C.copy()
+    Cg[7, 9] += 1e-3 * absab[7, 9]
+    assert abs(bench.componentwise_error(W, A, B, Cg, C) - 1e-3) <= 1e-9
