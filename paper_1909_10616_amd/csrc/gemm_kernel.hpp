@@ -922,10 +922,6 @@ __device__ __forceinline__ void gemm_fast_dl(const KArgs& a, char* smem) {
     acc[i][j] = mfma_bf16(__builtin_bit_cast(bf16x8, fa[fs][i]),
                           __builtin_bit_cast(bf16x8, fb[fs][j]), acc[i][j]);
   };
-  auto mfmas = [&](int fs) __attribute__((always_inline)) {
-#pragma unroll
-    for (int q = 0; q < TM * TN; ++q) mfma1(fs, q);
-  };
 
   // Ring schedule. Stage s is loaded into slot s mod ns. Its loads are issued
   // in a window of NCS chunk-steps of MFMAs: the last chunk-step of stage
@@ -956,7 +952,7 @@ __device__ __forceinline__ void gemm_fast_dl(const KArgs& a, char* smem) {
   auto run = [&](auto ni) __attribute__((always_inline)) {
     constexpr int NI = decltype(ni)::value;
     constexpr int NIE = NI ? NI : kMaxDlInst;
-    constexpr int RR = NI == kMaxDlInst ? 1 : (NI ? (SPOS / 2) / NI : (SPOS - TMTN / 2) / NIE);
+    constexpr int RR = NI == kMaxDlInst ? 1 : (NI ? (SPOS / 2) / (NI ? NI : 1) : (SPOS - TMTN / 2) / NIE);
     constexpr int R = RR > 1 ? RR : 1;
     // open: the window is open for every load of this stage (no guard on it)
     auto dma_at = [&](const StageBase& sb, bool on, int pos, auto open) __attribute__((always_inline)) {

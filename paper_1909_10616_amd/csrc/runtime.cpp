@@ -206,7 +206,7 @@ int measure(const gt_config& c, const void* A, const void* B, void* C, int64_t M
   std::vector<hipEvent_t> ev(static_cast<size_t>(runs) + 3, nullptr);
   auto destroy = [&]() {
     for (auto& x : ev)
-      if (x) hipEventDestroy(x);
+      if (x) (void)hipEventDestroy(x);
   };
   for (auto& x : ev) {
     hipError_t e = hipEventCreate(&x);
@@ -226,16 +226,16 @@ int measure(const gt_config& c, const void* A, const void* B, void* C, int64_t M
     return hip_fail(e, "hipEventRecord");
   }
   if ((rc = launch_lowered(lw, s)) != GT_OK) {
-    hipStreamSynchronize(s);
+    (void)hipStreamSynchronize(s);
     destroy();
     return rc;
   }
-  hipEventRecord(ev[1], s);
-  if ((e = hipEventSynchronize(ev[1])) != hipSuccess) {
+  if ((e = hipEventRecord(ev[1], s)) != hipSuccess || (e = hipEventSynchronize(ev[1])) != hipSuccess ||
+      (e = hipEventElapsedTime(&first, ev[0], ev[1])) != hipSuccess) {
+    (void)hipStreamSynchronize(s);
     destroy();
     return hip_fail(e, "warm-up run");
   }
-  hipEventElapsedTime(&first, ev[0], ev[1]);
   *first_ms = first;
   if (abort_ms > 0.0 && first > abort_ms) {
     *aborted = 1;
@@ -246,29 +246,41 @@ int measure(const gt_config& c, const void* A, const void* B, void* C, int64_t M
   }
   for (int w = 1; w < warmup; ++w)
     if ((rc = launch_lowered(lw, s)) != GT_OK) {
+      (void)hipStreamSynchronize(s);
       destroy();
       return rc;
     }
-  hipEventRecord(ev[2], s);
+  if ((e = hipEventRecord(ev[2], s)) != hipSuccess) {
+    (void)hipStreamSynchronize(s);
+    destroy();
+    return hip_fail(e, "hipEventRecord");
+  }
   for (int r = 0; r < runs; ++r) {
     if ((rc = launch_lowered(lw, s)) != GT_OK) {
-      hipStreamSynchronize(s);
+      (void)hipStreamSynchronize(s);
       destroy();
       return rc;
     }
-    hipEventRecord(ev[3 + r], s);
+    if ((e = hipEventRecord(ev[3 + r], s)) != hipSuccess) {
+      (void)hipStreamSynchronize(s);
+      destroy();
+      return hip_fail(e, "hipEventRecord");
+    }
   }
-  if ((e = hipEventSynchronize(ev[2 + runs])) != hipSuccess) {
+  if ((e = hipEventSynchronize(ev[2 + runs])) != hipSuccess ||
+      (e = hipEventElapsedTime(&total, ev[2], ev[2 + runs])) != hipSuccess) {
     destroy();
     return hip_fail(e, "timed runs");
   }
-  hipEventElapsedTime(&total, ev[2], ev[2 + runs]);
   *mean_ms = static_cast<double>(total) / runs;
   if (stats) {
     std::vector<double> d(static_cast<size_t>(runs));
     for (int r = 0; r < runs; ++r) {
       float ms = 0.0f;
-      hipEventElapsedTime(&ms, ev[2 + r], ev[3 + r]);
+      if ((e = hipEventElapsedTime(&ms, ev[2 + r], ev[3 + r])) != hipSuccess) {
+        destroy();
+        return hip_fail(e, "hipEventElapsedTime");
+      }
       d[r] = ms;
     }
     double var = 0.0;

@@ -165,18 +165,18 @@ struct Tuner {
   }
 
   int init(const gt_space* sp, const gt_tune_opts* opts, gt_cost_fn cb, void* cb_ctx,
-           gt_tune_result* res, const char* who) {
+           gt_tune_result* res, const char* caller) {
     if (int rc = make_space(sp, &s)) return rc;
     if (!opts || !res) {
-      set_error(std::string(who) + ": null options or result");
+      set_error(std::string(caller) + ": null options or result");
       return GT_EINVAL;
     }
     if (opts->budget < 1 || opts->rho < 1) {
-      set_error(std::string(who) + ": budget and rho must be >= 1");
+      set_error(std::string(caller) + ": budget and rho must be >= 1");
       return GT_EINVAL;
     }
     o = opts;
-    this->who = who;
+    who = caller;
     cost = cb;
     ctx = cb_ctx;
     out = res;
@@ -185,7 +185,7 @@ struct Tuner {
   }
 
   // GPU mode: operands, tolerance, and the reference product (once).
-  int prepare_gpu(const gt_space* sp, const char* who) {
+  int prepare_gpu(const gt_space* sp) {
     if (cost) return GT_OK;
     if (!o->A || !o->B || !o->C) {
       set_error(std::string(who) + ": GPU mode needs A, B and C");
@@ -270,7 +270,7 @@ struct Tuner {
   // After a device error that outlives its call: the result so far, and
   // GT_EHIP with the configuration that was being timed.
   bool fatal() const { return g.fatal != hipSuccess; }
-  int fail_fatal(const char* who, const gt_config& c, uint64_t best) {
+  int fail_fatal(const gt_config& c, uint64_t best) {
     finish(best);
     set_error(std::string(who) + ": device error while timing " + describe(c) + ": " +
               hipGetErrorString(g.fatal));
@@ -321,7 +321,7 @@ static int tune_gbfs_impl(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn 
     set_error("tune_gbfs: s0 is not legitimate");
     return GT_EILLEGIT;
   }
-  if (int rc = t.prepare_gpu(sp, "tune_gbfs")) return rc;
+  if (int rc = t.prepare_gpu(sp)) return rc;
 
   using Item = std::pair<double, uint64_t>;  // (cost, rank), smallest first
   std::priority_queue<Item, std::vector<Item>, std::greater<Item>> q;
@@ -333,7 +333,7 @@ static int tune_gbfs_impl(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn 
   visited.insert(r0);
   t.cost_min = c0;
   uint64_t best = r0;
-  if (t.fatal()) return t.fail_fatal("tune_gbfs", s0, best);
+  if (t.fatal()) return t.fail_fatal(s0, best);
   if (!std::isinf(c0)) q.push({c0, r0});
 
   out->stop_reason = 1;
@@ -373,7 +373,7 @@ static int tune_gbfs_impl(const gt_space* sp, const gt_tune_opts* o, gt_cost_fn 
         continue;
       }
       const double v = t.time_one(g_s[i], r);
-      if (t.fatal()) return t.fail_fatal("tune_gbfs", g_s[i], best);
+      if (t.fatal()) return t.fail_fatal(g_s[i], best);
       visited.insert(r);
       if (!std::isinf(v)) q.push({v, r});
       if (v < t.cost_min) {
@@ -392,7 +392,7 @@ static int tune_random_impl(const gt_space* sp, const gt_tune_opts* o, gt_cost_f
   using namespace gt;
   Tuner t;
   if (int rc = t.init(sp, o, cost, ctx, out, "tune_random")) return rc;
-  if (int rc = t.prepare_gpu(sp, "tune_random")) return rc;
+  if (int rc = t.prepare_gpu(sp)) return rc;
   const Space& s = t.s;
   std::unordered_set<uint64_t> visited;
   uint64_t rng = o->seed;
@@ -427,7 +427,7 @@ static int tune_random_impl(const gt_space* sp, const gt_tune_opts* o, gt_cost_f
     }
     visited.insert(r);
     const double v = t.time_one(c, r);
-    if (t.fatal()) return t.fail_fatal("tune_random", c, best);
+    if (t.fatal()) return t.fail_fatal(c, best);
     if (!have || v < t.cost_min) {
       t.cost_min = v;
       best = r;
@@ -687,7 +687,7 @@ static int tune_na2c_impl(const gt_space* sp, const gt_tune_opts* o, const gt_na
     set_error("tune_na2c: s0 is not a legitimate member of the space");
     return is_member(s, s0) ? GT_EILLEGIT : GT_EDIMS;
   }
-  if (int rc = t.prepare_gpu(sp, "tune_na2c")) return rc;
+  if (int rc = t.prepare_gpu(sp)) return rc;
 
   Agent agent(s, p, o->seed);
   const int A = agent.actions();
@@ -701,7 +701,7 @@ static int tune_na2c_impl(const gt_space* sp, const gt_tune_opts* o, const gt_na
   hv[r0] = c0;
   t.cost_min = c0;
   uint64_t best = r0;
-  if (t.fatal()) return t.fail_fatal("tune_na2c", s0, best);
+  if (t.fatal()) return t.fail_fatal(s0, best);
   gt_config centre = s0;
 
   out->stop_reason = 1;
@@ -773,7 +773,7 @@ static int tune_na2c_impl(const gt_space* sp, const gt_tune_opts* o, const gt_na
     }
     for (size_t b = 0; b < coll.size() && out->timed < o->budget; ++b) {
       const double c = t.time_one(coll[b], coll_r[b]);
-      if (t.fatal()) return t.fail_fatal("tune_na2c", coll[b], best);
+      if (t.fatal()) return t.fail_fatal(coll[b], best);
       if (c < t.cost_min) {
         t.cost_min = c;
         best = coll_r[b];
