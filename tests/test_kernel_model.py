@@ -83,6 +83,21 @@ def a_read_slot(I, BM, CPR, row, grp, cs):
     return (xa ^ (c & 7)) + (c & ~7)
 
 
+def fast_slot(idx, rows, I, CPR):
+    """LDS slot of chunk idx = row·CPR + chunk of a register-staged tile (A
+    [m][k] or B stored [n][k]): the stage-wide layout, swizzled."""
+    return swz(idx)
+
+
+def fast_read_slot(row, grp, c, CPR):
+    """LDS slot a lane of the register-staged path reads for row `row`, chunk
+    c + grp (c = chunk-step·G), as the kernel computes it: a per-row base for
+    the 128-byte line of the chunk-step, then the chunk-step's XOR and line."""
+    j = (c >> 3) if CPR >= 8 else 0
+    x = swz((row << lg(CPR)) + grp + 8 * j) - 8 * j
+    return (x ^ (c & 7)) + (c & ~7)
+
+
 def lg(v):
     r = v.bit_length() - 1
     assert 1 << r == v
@@ -132,17 +147,22 @@ def frag_steps(L, CPR, lane):
 
 
 def check_c_and_frags(L, CPR, achunks, lane, bt_rows=None, a_slots=True):
+    """Fragment reads of the register-staged path (A, and B stored [n][k]
+    like A): each lane's slot is in the tile and is the slot its chunk
+    (row, chunk-step·G + lane group) was written to."""
     I = L["I"]
     for w, wm, wn, c, j, LGCPR, grp in frag_steps(L, CPR, lane):
         for t in range(L["TM"] if a_slots else 0):
-            q0 = ((wm * L["WM"] + t * I + lane % I) << LGCPR) + grp + 8 * j
-            idx = ((swz(q0) - 8 * j) ^ (c & 7)) + (c & ~7)
+            row = wm * L["WM"] + t * I + lane % I
+            idx = fast_read_slot(row, grp, c, CPR)
             assert idx.min() >= 0 and idx.max() < achunks
-        if bt_rows is not None:  # register-staged path: B stored [n][k] like A
+            assert np.array_equal(idx, fast_slot((row << LGCPR) + c + grp, L["BM"], I, CPR))
+        if bt_rows is not None:
             for t in range(L["TN"]):
-                q0 = ((wn * L["WN"] + t * I + lane % I) << LGCPR) + grp + 8 * j
-                idx = ((swz(q0) - 8 * j) ^ (c & 7)) + (c & ~7)
+                row = wn * L["WN"] + t * I + lane % I
+                idx = fast_read_slot(row, grp, c, CPR)
                 assert idx.min() >= 0 and idx.max() < bt_rows << LGCPR
+                assert np.array_equal(idx, fast_slot((row << LGCPR) + c + grp, bt_rows, I, CPR))
     for w in range(L["W"]):
         wm, wn = w % L["wavesM"], w // L["wavesM"]
         for e in range(I * I // 64):
@@ -155,6 +175,7 @@ def check_c_and_frags(L, CPR, achunks, lane, bt_rows=None, a_slots=True):
 
 def check_fast(L, info, M, N, K, vec=8, akm=False):
     VEC, LGV = vec, lg(vec)
+    I = L["I"]
     CPR = L["BK"] // VEC
     LGCPR = lg(CPR)
     nthr = 64 * L["W"]
@@ -182,28 +203,39 @@ def check_fast(L, info, M, N, K, vec=8, akm=False):
             for j in range(VEC):
                 addr = gm * BM + (kbase + (kb << LGV) + j) * M + (nm << LGV)
                 assert addr.min() >= 0 and addr.max() + VEC <= K * M
-                assert swz((((nm << LGV) + j) << LGCPR) + kb).max() < achunks
-            # every A chunk of the stage is written
-            dst = np.concatenate([swz((((nm << LGV) + j) << LGCPR) + kb) for j in range(VEC)])
+                assert fast_slot((((nm << LGV) + j) << LGCPR) + kb, BM, I, CPR).max() < achunks
+            # every A chunk of the stage is written, each to its own slot
+            dst = np.concatenate([fast_slot((((nm << LGV) + j) << LGCPR) + kb, BM, I, CPR)
+                                  for j in range(VEC)])
             assert len(np.unique(dst)) == achunks
         elif prefetch:
             ta = np.minimum(tid, achunks - 1)
             na = min(8, -(-achunks // nthr))
+            dst = []
             for i in range(na):
                 e = ta + i * nthr
                 addr = a0 + (ta >> LGCPR) * K + ((ta & (CPR - 1)) << LGV) + i * (nthr >> LGCPR) * K
                 assert addr.min() >= 0 and addr.max() + VEC <= M * K
-                assert swz(e).max() < achunks
+                # the chunk at addr is row e / CPR, chunk e mod CPR of the tile
+                assert np.array_equal(addr, a0 + (e >> LGCPR) * K + ((e & (CPR - 1)) << LGV))
+                dst.append(fast_slot(e, BM, I, CPR))
+            dst = np.concatenate(dst)
+            assert dst.max() < achunks and len(np.unique(dst)) == achunks
         else:
             e = np.arange(achunks)
             addr = a0 + (e >> LGCPR) * K + ((e & (CPR - 1)) << LGV)
-            assert addr.max() + VEC <= M * K and swz(e).max() < achunks
+            dst = fast_slot(e, BM, I, CPR)
+            assert addr.max() + VEC <= M * K and dst.max() < achunks
+            assert len(np.unique(dst)) == achunks
         b = np.minimum(tid, bblocks - 1) if prefetch else np.arange(bblocks)
         nb, kb = b & ((1 << lgnbn) - 1), b >> lgnbn
+        bdst = []
         for j in range(VEC):
             addr = b0 + ((kb << LGV) + j) * N + (nb << LGV)
             assert addr.min() >= 0 and addr.max() + VEC <= K * N
-            assert swz((((nb << LGV) + j) << LGCPR) + kb).max() < BN << LGCPR
+            bdst.append(fast_slot((((nb << LGV) + j) << LGCPR) + kb, BN, I, CPR))
+        bdst = np.concatenate(bdst)
+        assert bdst.max() < BN << LGCPR and len(np.unique(bdst)) == BN << LGCPR
     check_c_and_frags(L, CPR, achunks, np.arange(64), bt_rows=BN)
 
 
