@@ -63,3 +63,55 @@ def test_random_spaces_match_oracle(sides, case):
         assert ls.rank(c) == r == os_.rank(c)
         assert ls.legit(c) == os_.legit(c), (args, c)
         assert ls.neighbours(c) == os_.neighbours(c), (args, mode, c)
+
+
+def _splitmix_cost(seed, inf_mod):
+    """A synthetic cost keyed by rank (after the paper's random-reward
+    experiment): 1 + SplitMix64(rank ⊕ seed) / 2^64, and +∞ for every rank
+    ≡ 5 (mod inf_mod) when inf_mod > 0 (a failed candidate)."""
+    M64 = (1 << 64) - 1
+
+    def f(cfg, rank):
+        if inf_mod and rank % inf_mod == 5:
+            return float("inf")
+        z = ((rank ^ seed) + 0x9E3779B97F4A7C15) & M64
+        z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & M64
+        z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & M64
+        return 1.0 + (z ^ (z >> 31)) / 2.0 ** 64
+    return f
+
+
+@st.composite
+def searches(draw):
+    args, mode, fracs = draw(spaces())
+    rho = draw(st.integers(1, 8))
+    budget = draw(st.integers(1, 300))
+    seed = draw(st.integers(0, (1 << 32) - 1))
+    inf_mod = draw(st.sampled_from([0, 7, 11]))
+    return args, mode, fracs, rho, budget, seed, inf_mod
+
+
+@settings(max_examples=150, deadline=None, suppress_health_check=[HealthCheck.function_scoped_fixture])
+@given(searches())
+def test_random_searches_match_oracle(sides, case):
+    """G-BFS (Alg.1) from a drawn legitimate start, and the equal-budget
+    random search, under synthetic costs with failures: the same ordered
+    list of timed ranks, the same s*, cost, count timed and pops."""
+    gt, orc = sides
+    args, mode, fracs, rho, budget, seed, inf_mod = case
+    ls, os_ = gt.Space(*args, mode=mode), orc.Space(*args, mode=mode)
+    size = ls.size()
+    starts = [ls.unrank(int(f * size)) for f in fracs] + [ls.paper_s0()]
+    s0 = next((c for c in starts if ls.legit(c)), None)
+    cost = _splitmix_cost(seed, inf_mod)
+    if s0 is not None:
+        got = gt.tune_gbfs(ls, budget=budget, s0=s0, rho=rho, seed=seed, cost_fn=cost)
+        exp = orc.gbfs(os_, s0, rho, budget, seed, cost)
+        assert [e["rank"] for e in got["log"]] == exp["log_ranks"], (args, mode, s0, rho, seed)
+        assert got["best"] == exp["best"] and got["best_cost"] == exp["best_cost"]
+        assert got["timed"] == exp["timed"] and got["popped"] == exp["popped"]
+    got = gt.tune_random(ls, budget=budget, seed=seed, cost_fn=cost)
+    exp = orc.random_search(os_, budget, seed, cost)
+    assert [e["rank"] for e in got["log"]] == exp["log_ranks"], (args, seed)
+    assert got["best"] == exp["best"] and got["best_cost"] == exp["best_cost"]
+    assert got["timed"] == exp["timed"] and got["popped"] == exp["popped"]
