@@ -309,7 +309,8 @@ int gt_na2c_params_init(gt_na2c_params* p);
  * from the centre (s0, then the best state so far) until B unvisited
  * legitimate states are collected (illegitimate states may be walked
  * through, never collected) or max_walks walks were made; with probability
- * eps a step samples π, else a uniform available action (SplitMix64(seed)).
+ * eps a step samples π, else a uniform available action (SplitMix64(seed));
+ * a walk ends at a state with no available action (one-configuration spaces).
  * An episode that collects nothing lengthens the walks by one step (the
  * paper lets the exploration step grow; params->eps_halving also halves eps),
  * up to T + 8 steps, after which the search stops (stop_reason 1); a new best

@@ -848,13 +848,15 @@ static int params_bad(const or_na2c_params* p) {
 
 /* a ∈ 𝒜 drawn for one walk step in s: with probability ε from π(·|s)
  * (inverse CDF over the available actions in list order), else uniformly
- * among the available ones */
+ * among the available ones; -1, drawing nothing, when no action is
+ * available in s (the walk ends there) */
 static int na_pick(const or_space* sp, const na_shape* z, const double* tha, const or_config* s,
                    double eps, uint64_t* rng) {
   int ok[NA_MAXA];
   na_ok_all(z, s, ok);
   int n_ok = 0;
   for (int b = 0; b < z->A; ++b) n_ok += ok[b];
+  if (n_ok == 0) return -1;
   if (unit_draw(rng) < eps) {
     double phi[NA_MAXF], h[NA_MAXH], pi[NA_MAXA];
     na_phi(sp, z, s, phi);
@@ -932,6 +934,7 @@ int or_na2c(const or_space* sp, const or_config* s0, const or_na2c_params* prm,
       or_config s = centre;
       for (int t = 0; t < walk; ++t) {
         const int a = na_pick(sp, &z, tha, &s, eps, &rng);
+        if (a < 0) break; /* a dead end: no move leaves s */
         const or_config s2 = na_move(&z, &s, a);
         if (or_legit(sp, &s2) && nb < prm->B) {
           uint64_t r2;

@@ -728,6 +728,7 @@ static int tune_na2c_impl(const gt_space* sp, const gt_tune_opts* o, const gt_na
       for (int step = 0; step < walk; ++step) {
         int navail = 0;
         for (int a = 0; a < A; ++a) navail += (avail[a] = agent.available(cur, a) ? 1 : 0);
+        if (navail == 0) break;  // no move leaves cur: the walk ends, nothing drawn
         int act = -1;
         if (Agent::uniform(&rng) < eps_now) {
           agent.features(cur, phi);

@@ -326,6 +326,25 @@ def test_tune_na2c_synthetic_trajectory_matches_oracle(gt, orc, case, cost_kind)
     assert res["best"] == ref["best"] and res["best_cost"] == ref["best_cost"]
 
 
+@pytest.mark.parametrize("args", [(3, 5, 7, (2, 2, 2), "f32", False),
+                                  (64, 32, 64, (1, 1, 1), "bf16", False)])
+@pytest.mark.parametrize("params", [None, {"eps": 1.0}, {"eps": 0.0, "eps_halving": 1}])
+def test_tune_na2c_on_a_space_without_moves(gt, orc, args, params):
+    """A space of one configuration and no MFMA coordinate offers no action
+    in any state: every walk ends where it starts, so N-A2C times s0, spends
+    the episodes T … T+8 finding nothing and stops (the library and the
+    oracle once divided by the zero count of available actions here)."""
+    sp, osp = gt.Space(*args), orc.Space(*args)
+    assert sp.size() == 1 and sp.neighbours(sp.unrank(0)) == []
+    s0 = sp.unrank(0)
+    cost = lambda c, r: 2.5   # noqa: E731
+    res = gt.tune_na2c(sp, 40, s0=s0, seed=11, cost_fn=cost, params=params)
+    ref = orc.na2c(osp, s0, 40, 11, cost, params)
+    assert res["timed"] == ref["timed"] == 1 and res["best"] == ref["best"] == s0
+    assert res["popped"] == ref["popped"] == 9
+    assert res["stop_reason"] == "neighbourhood-exhausted"
+
+
 def test_tune_na2c_errors(gt):
     sp = gt.Space(256, 256, 256, (3, 3, 3), "f32", False)
     for bad in ({"T": 0}, {"B": 0}, {"H": 65}, {"mem": 0}, {"max_walks": 0}, {"eps": 1.5},

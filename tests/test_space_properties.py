@@ -3,7 +3,9 @@ drawn spaces (§3.3 Eq.1–4, §4.1 Eq.5–9): extents with odd cofactors, one t
 four levels per dimension, both dtypes, with and without the MFMA
 coordinate, both neighbour relations. For every drawn space the library and
 the oracle agree on |ξ|, and at drawn ranks on unrank, rank, legitimacy and
-the neighbour list; a space one side rejects the other rejects too."""
+the neighbour list; a space one side rejects the other rejects too. On
+drawn spaces, starts, budgets, seeds and settings, G-BFS (Alg.1), the random
+search and N-A2C (Alg.2) time the oracle's sequence of configurations."""
 import pytest
 from hypothesis import HealthCheck, given, settings
 from hypothesis import strategies as st
@@ -113,5 +115,45 @@ def test_random_searches_match_oracle(sides, case):
     got = gt.tune_random(ls, budget=budget, seed=seed, cost_fn=cost)
     exp = orc.random_search(os_, budget, seed, cost)
     assert [e["rank"] for e in got["log"]] == exp["log_ranks"], (args, seed)
+    assert got["best"] == exp["best"] and got["best_cost"] == exp["best_cost"]
+    assert got["timed"] == exp["timed"] and got["popped"] == exp["popped"]
+
+
+@st.composite
+def na2c_runs(draw):
+    args, mode, fracs = draw(spaces())
+    params = {
+        "T": draw(st.integers(1, 5)), "B": draw(st.integers(1, 16)), "H": draw(st.integers(1, 64)),
+        "mem": draw(st.integers(1, 512)), "max_walks": draw(st.integers(1, 96)),
+        "reward": draw(st.integers(0, 1)), "eps_halving": draw(st.integers(0, 1)),
+        "eps": draw(st.floats(0.0, 1.0)), "gamma": draw(st.floats(0.0, 1.0)),
+        "lr": draw(st.floats(1e-4, 0.2)), "r_clip": draw(st.floats(0.25, 10.0)),
+    }
+    budget = draw(st.integers(1, 150))
+    seed = draw(st.integers(0, (1 << 32) - 1))
+    inf_mod = draw(st.sampled_from([0, 7, 11]))
+    return args, mode, fracs, params, budget, seed, inf_mod
+
+
+@settings(max_examples=80, deadline=None, suppress_health_check=[HealthCheck.function_scoped_fixture])
+@given(na2c_runs())
+def test_random_na2c_runs_match_oracle(sides, case):
+    """N-A2C (§4.3, Alg.2) from a drawn legitimate start with drawn settings
+    (walk length, batch, hidden width, memory, ε, γ, learning rate, both
+    rewards, ε halving) under synthetic costs with failures: the same timed
+    ranks and costs, s*, count timed and episodes, bit for bit."""
+    gt, orc = sides
+    args, mode, fracs, params, budget, seed, inf_mod = case
+    ls, os_ = gt.Space(*args, mode=mode), orc.Space(*args, mode=mode)
+    size = ls.size()
+    starts = [ls.unrank(int(f * size)) for f in fracs] + [ls.paper_s0()]
+    s0 = next((c for c in starts if ls.legit(c)), None)
+    if s0 is None:
+        return
+    cost = _splitmix_cost(seed, inf_mod)
+    got = gt.tune_na2c(ls, budget, s0=s0, seed=seed, cost_fn=cost, params=params)
+    exp = orc.na2c(os_, s0, budget, seed, cost, params)
+    assert [e["rank"] for e in got["log"]] == exp["log_ranks"], (args, mode, s0, params, seed)
+    assert [e["cost_ms"] for e in got["log"]] == exp["log_costs"]
     assert got["best"] == exp["best"] and got["best_cost"] == exp["best_cost"]
     assert got["timed"] == exp["timed"] and got["popped"] == exp["popped"]
