@@ -198,7 +198,7 @@ typedef struct gt_log_entry {
 } gt_log_entry;
 
 /* Synthetic cost (the CPU "fake backend"): returns the cost of cfg, +inf for
- * a failure. */
+ * a failure. A NaN is taken as +inf (logged as such, counted in `failed`). */
 typedef double (*gt_cost_fn)(const gt_config* cfg, uint64_t rank, void* ctx);
 
 typedef struct gt_tune_opts {

@@ -439,6 +439,14 @@ uint64_t or_splitmix64_next(uint64_t* state) {
 /* G-BFS (§4.2, Alg.1).                                                      */
 /* ------------------------------------------------------------------------ */
 
+/* cost(s) of one candidate (§4.2: its measured run time). A value that is
+ * not a number is no measurement: the candidate counts as failed, +∞, as a
+ * launch that fails does. */
+static double measured(or_cost_fn cost, or_config* c, uint64_t rank, void* ctx) {
+  const double v = cost(c, rank, ctx);
+  return isnan(v) ? INFINITY : v;
+}
+
 int or_gbfs(const or_space* sp, const or_config* s0, int rho, int64_t budget,
             uint64_t seed, or_cost_fn cost, void* ctx, or_gbfs_result* res,
             uint64_t* log_ranks, double* log_costs, int64_t log_cap) {
@@ -460,7 +468,7 @@ int or_gbfs(const or_space* sp, const or_config* s0, int rho, int64_t budget,
   uint64_t r0;
   rank_with(sp, &tb, s0, &r0);
   or_config s0c = *s0;
-  double c0 = cost(&s0c, r0, ctx);
+  double c0 = measured(cost, &s0c, r0, ctx);
   if (timed < log_cap) {
     log_ranks[timed] = r0;
     log_costs[timed] = c0;
@@ -503,7 +511,7 @@ int or_gbfs(const or_space* sp, const or_config* s0, int rho, int64_t budget,
       rank_with(sp, &tb, &g[i], &r);
       if (!g[i].legit) continue;
       if (vis[r / 8] & (1u << (r % 8))) continue;
-      const double c = cost(&g[i], r, ctx);
+      const double c = measured(cost, &g[i], r, ctx);
       if (timed < log_cap) {
         log_ranks[timed] = r;
         log_costs[timed] = c;
@@ -559,7 +567,7 @@ int or_random_search(const or_space* sp, int64_t budget, uint64_t seed, or_cost_
     if (!or_legit(sp, &c)) continue;
     if (vis[r / 8] & (1u << (r % 8))) continue;
     vis[r / 8] |= (unsigned char)(1u << (r % 8));
-    const double v = cost(&c, r, ctx);
+    const double v = measured(cost, &c, r, ctx);
     if (timed < log_cap) {
       log_ranks[timed] = r;
       log_costs[timed] = v;
@@ -915,7 +923,7 @@ int or_na2c(const or_space* sp, const or_config* s0, const or_na2c_params* prm,
   uint64_t r0;
   rank_with(sp, &tb, s0, &r0);
   or_config first = *s0;
-  const double c0 = cost(&first, r0, ctx);
+  const double c0 = measured(cost, &first, r0, ctx);
   if (timed < log_cap) log_ranks[timed] = r0, log_costs[timed] = c0;
   ++timed;
   uint64_t slot = na_find(&hv, r0);
@@ -955,7 +963,7 @@ int or_na2c(const or_space* sp, const or_config* s0, const or_na2c_params* prm,
     }
     for (int b = 0; b < nb && timed < budget; ++b) {
       or_config sb = batch[b];
-      const double c = cost(&sb, batch_r[b], ctx);
+      const double c = measured(cost, &sb, batch_r[b], ctx);
       if (timed < log_cap) log_ranks[timed] = batch_r[b], log_costs[timed] = c;
       ++timed;
       if (c < cost_min) { /* new s*: the next episode walks from it */

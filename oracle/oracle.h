@@ -74,6 +74,7 @@ int or_neighbours(const or_space* sp, const or_config* s, or_config* out,
 
 uint64_t or_splitmix64_next(uint64_t* state);
 
+/* cost of a candidate; +∞ marks a failure, and a NaN is taken as +∞ */
 typedef double (*or_cost_fn)(const or_config* c, uint64_t rank, void* ctx);
 typedef struct {
   or_config best;

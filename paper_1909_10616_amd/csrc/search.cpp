@@ -236,6 +236,7 @@ struct Tuner {
     const auto te = std::chrono::steady_clock::now();
     if (cost) {
       v = cost(&c, rank, ctx);
+      if (std::isnan(v)) v = INFINITY;  // no number, no measurement: a failed candidate
       rec.cost_ms = v;
       rec.first_ms = v;
       rec.rel_err = NAN;

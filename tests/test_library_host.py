@@ -326,6 +326,35 @@ def test_tune_na2c_synthetic_trajectory_matches_oracle(gt, orc, case, cost_kind)
     assert res["best"] == ref["best"] and res["best_cost"] == ref["best_cost"]
 
 
+@pytest.mark.parametrize("search", ["gbfs", "random", "na2c"])
+def test_nan_cost_is_a_failed_candidate(gt, orc, search):
+    """A cost that is not a number is no measurement: the library and the
+    oracle both take it as +∞ (a failed candidate), log it as such and count
+    it in `failed`; G-BFS used to order its queue by the NaN itself and left
+    the oracle's trajectory."""
+    sp = gt.Space(256, 256, 256, (3, 3, 3), "f32", False)
+    osp = orc.Space(256, 256, 256, (3, 3, 3), "f32", False)
+
+    def cost(c, r):
+        h = (r * 2654435761) % 997
+        return float("nan") if h % 5 == 0 else 1.0 + h / 997
+
+    s0 = sp.paper_s0()
+    if search == "gbfs":
+        res, ref = gt.tune_gbfs(sp, 150, s0=s0, rho=3, seed=4, cost_fn=cost), \
+            orc.gbfs(osp, s0, 3, 150, 4, cost)
+    elif search == "random":
+        res, ref = gt.tune_random(sp, 150, seed=4, cost_fn=cost), orc.random_search(osp, 150, 4, cost)
+    else:
+        res, ref = gt.tune_na2c(sp, 150, s0=s0, seed=4, cost_fn=cost), orc.na2c(osp, s0, 150, 4, cost)
+    costs = [e["cost_ms"] for e in res["log"]]
+    assert [e["rank"] for e in res["log"]] == ref["log_ranks"] and costs == ref["log_costs"]
+    assert res["best"] == ref["best"] and res["best_cost"] == ref["best_cost"]
+    nan_ranks = [e["rank"] for e in res["log"] if (e["rank"] * 2654435761) % 997 % 5 == 0]
+    assert nan_ranks and res["failed"] == len(nan_ranks) == costs.count(math.inf)
+    assert all(e["status"] == "launch-failure" for e in res["log"] if e["rank"] in nan_ranks)
+
+
 @pytest.mark.parametrize("args", [(3, 5, 7, (2, 2, 2), "f32", False),
                                   (64, 32, 64, (1, 1, 1), "bf16", False)])
 @pytest.mark.parametrize("params", [None, {"eps": 1.0}, {"eps": 0.0, "eps_halving": 1}])

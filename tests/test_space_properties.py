@@ -69,13 +69,16 @@ def test_random_spaces_match_oracle(sides, case):
 
 def _splitmix_cost(seed, inf_mod):
     """A synthetic cost keyed by rank (after the paper's random-reward
-    experiment): 1 + SplitMix64(rank ⊕ seed) / 2^64, and +∞ for every rank
-    ≡ 5 (mod inf_mod) when inf_mod > 0 (a failed candidate)."""
+    experiment): 1 + SplitMix64(rank ⊕ seed) / 2^64, and when inf_mod > 0
+    +∞ for every rank ≡ 5 and NaN for every rank ≡ 3 (mod inf_mod): two
+    ways a candidate fails."""
     M64 = (1 << 64) - 1
 
     def f(cfg, rank):
         if inf_mod and rank % inf_mod == 5:
             return float("inf")
+        if inf_mod and rank % inf_mod == 3:
+            return float("nan")
         z = ((rank ^ seed) + 0x9E3779B97F4A7C15) & M64
         z = ((z ^ (z >> 30)) * 0xBF58476D1CE4E5B9) & M64
         z = ((z ^ (z >> 27)) * 0x94D049BB133111EB) & M64
