@@ -60,7 +60,7 @@ typedef enum { GT_ADJACENT = 0, GT_ANY_PAIR = 1 } gt_neighbour_mode;
  * neighbour_mode: GT_ADJACENT moves a factor of 2 between adjacent levels;
  * GT_ANY_PAIR between any two levels (§4.1 Eq.6 as printed). */
 typedef struct gt_space {
-  int64_t M, N, K;
+  int64_t M, N, K;         /* 1..2^40; a space outside these ranges is GT_EINVAL */
   int32_t d_m, d_k, d_n;   /* 1..GT_MAXD */
   int32_t dtype;           /* gt_dtype of A and B (| GT_A_KMAJOR); C is fp32 */
   int32_t mfma_coord;      /* 0 or 1 */

@@ -156,11 +156,17 @@ static int64_t sp_ext(const or_space* sp, int x) {
   return x == 0 ? sp->M : (x == 1 ? sp->K : sp->N);
 }
 
+/* the domain of a space: extents 1..2^40, 1..4 levels, a known dtype,
+ * a 0/1 MFMA coordinate flag and one of the two neighbour relations */
 static int sp_ok(const or_space* sp) {
   if (!sp) return 0;
   for (int x = 0; x < 3; ++x)
-    if (sp->d[x] < 1 || sp->d[x] > OR_MAXD || sp_ext(sp, x) < 1) return 0;
-  return 1;
+    if (sp->d[x] < 1 || sp->d[x] > OR_MAXD || sp_ext(sp, x) < 1 ||
+        sp_ext(sp, x) > ((int64_t)1 << 40))
+      return 0;
+  return (sp->dtype == OR_F32 || sp->dtype == OR_BF16) &&
+         (sp->mfma_coord == 0 || sp->mfma_coord == 1) &&
+         (sp->mode == OR_ADJACENT || sp->mode == OR_ANY_PAIR);
 }
 
 /* Per-dimension tuple tables, built fresh for each call (plain, not fast). */
