@@ -13,9 +13,11 @@ built with gcc) through ctypes and shares no code with the GPU library:
   (§4.3), with ``na2c_probe`` / ``na2c_train`` exposing its networks and
   its training step.
 
-Parity unpinned: the hardware part of J (register, LDS and grid limits) has
-no value in the paper to pin it; it is checked by hand-worked cases and by
-every J=1 configuration launching on the GPU.
+The hardware part of J (register, LDS and grid limits) has no value in the
+paper to pin it; it is checked by hand-worked cases, by every J=1
+configuration launching on the GPU, and in one direction against the
+compiled kernels' metadata (whatever J admits fits the kernel it launches);
+where exactly J draws its line has nothing outside it to pin to.
 """
 from __future__ import annotations
 

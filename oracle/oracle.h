@@ -15,9 +15,12 @@
  *     training step exposed for pinning (or_na2c_probe, or_na2c_train).
  *
  * Parity pins: see tests/test_oracle_*.py. The legitimacy predicate beyond
- * membership (the hardware constraints) has no paper pin: "parity unpinned"
- * as to its hardware meaning; it is pinned only by hand-worked cases and by
- * every J=1 configuration launching on the GPU.
+ * membership (the hardware constraints) has no paper value: it is pinned by
+ * hand-worked cases, by every J=1 configuration launching on the GPU, and in
+ * one direction by the compiled kernels themselves (every configuration it
+ * admits fits the register allocation, largest workgroup and LDS that the
+ * gfx950 code objects record); where exactly it draws the line is a design
+ * choice with nothing outside to pin it to.
  */
 #ifndef GEMM_ORACLE_H
 #define GEMM_ORACLE_H

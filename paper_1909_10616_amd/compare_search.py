@@ -1,7 +1,7 @@
 """G-BFS against equal-budget random search, several seeds, one GPU (§5).
 
   python -m paper_1909_10616_amd.compare_search --workload gemm4096_bf16 --seeds 10
-      [--budget N] [--t-max S] [--s0 hand|paper] [--out FILE.json]
+      [--budget N] [--t-max S] [--s0 hand|paper] [--methods gbfs,random] [--out FILE.json]
 
 For every seed both searches run on the same resident inputs and the same
 reference product (computed once); every candidate is timed the same way
@@ -33,12 +33,17 @@ def main():
     ap.add_argument("--t-max", type=float, default=0.0)
     ap.add_argument("--s0", choices=["hand", "paper"], default="hand")
     ap.add_argument("--rho", type=int, default=5)
+    ap.add_argument("--methods", default="gbfs,random",
+                    help="comma-separated subset of gbfs,random (random search has no s0)")
     ap.add_argument("--out", default=None)
     ap.add_argument("--progress", type=float, default=0.0,
                     help="> 0: a progress line on stderr at most this often (s)")
     ap.add_argument("--trace", action="store_true",
                     help="name every candidate on stderr before it is launched")
     args = ap.parse_args()
+    methods = [m for m in args.methods.split(",") if m]
+    if not methods or any(m not in ("gbfs", "random") for m in methods):
+        raise SystemExit("--methods: a comma-separated subset of gbfs,random")
 
     import torch
     from paper_1909_10616_amd import gemmtune as gt
@@ -62,6 +67,8 @@ def main():
     for seed in range(args.seeds):
         row = {"seed": seed}
         for name, fn in (("gbfs", gt.tune_gbfs), ("random", gt.tune_random)):
+            if name not in methods:
+                continue
             # every candidate is named on stderr before it is launched
             kw = dict(budget=budget, seed=seed, t_max_s=args.t_max, A=Ad, B=Bd, C=C, c_ref=R,
                       trace_fd=2 if args.trace else -1, progress_s=args.progress)
@@ -84,7 +91,7 @@ def main():
 
     summary = {"workload": w.name, "budget": budget, "t_max_s": args.t_max, "s0": gt.fmt_cfg(s0),
                "s0_kind": args.s0, "space_size": sp.size(), "seeds": args.seeds,
-               "gbfs": stats("gbfs"), "random": stats("random"), "runs": runs}
+               **{m: stats(m) for m in methods}, "runs": runs}
     print(json.dumps({k: v for k, v in summary.items() if k != "runs"}), flush=True)
     if args.out:
         with open(args.out, "w") as f:
