@@ -18,6 +18,11 @@
  *     per kernel and hold no memory.
  *   - Space functions (gt_space_size … neighbours) are pure host code, need no
  *     GPU and are thread-safe.
+ *   - gemm_run, gt_measure, gt_reference_gemm, gt_compare and the searches may
+ *     be called from several host threads at once: each works on the caller's
+ *     buffers and stream, and the comparisons take the per-GPU result buffer
+ *     in turn. The exception is gt_compare_noalloc, whose calls on one GPU
+ *     share one scratch array and must not overlap.
  *   - Dimension order is m, k, n everywhere, as in the paper's configuration
  *     (§3.3 Eq.1) and state (§4.1 Eq.5).
  */

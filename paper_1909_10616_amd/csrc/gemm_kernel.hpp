@@ -19,6 +19,7 @@
 #pragma once
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cstdint>
 #include <type_traits>
 
@@ -1119,14 +1120,21 @@ __global__ void __launch_bounds__((launch_threads<I, TM, TN, CPR>())) gemm_kerne
 
 using LaunchFn = hipError_t (*)(const KArgs&, dim3, dim3, size_t, hipStream_t);
 
+// Raises the kernel's dynamic LDS limit once per device (bit d of `attr_devs`
+// for device d < 64; beyond that on every launch), then launches. Concurrent
+// callers may both set the attribute, which is idempotent.
 template <class F>
-hipError_t launch_one(F fn, bool& attr_set, const KArgs& a, dim3 grid, dim3 block, size_t lds,
-                      hipStream_t s) {
-  if (!attr_set) {  // raise the dynamic LDS limit once per kernel
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, 163840);
+hipError_t launch_one(F fn, std::atomic<uint64_t>& attr_devs, const KArgs& a, dim3 grid,
+                      dim3 block, size_t lds, hipStream_t s) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const uint64_t bit = dev >= 0 && dev < 64 ? uint64_t{1} << dev : 0;
+  if (!bit || !(attr_devs.load(std::memory_order_acquire) & bit)) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, 163840);
     if (e != hipSuccess) return e;
-    attr_set = true;
+    attr_devs.fetch_or(bit, std::memory_order_release);
   }
   hipLaunchKernelGGL(fn, grid, block, lds, s, a);
   return hipGetLastError();
@@ -1138,16 +1146,16 @@ template <int DT, int I, int TM, int TN, int CPR, bool AKM = false>
 hipError_t launch_gemm(const KArgs& a, dim3 grid, dim3 block, size_t lds, hipStream_t s) {
   if constexpr (AKM) {
     static_assert(CPR > 0, "the K-major-A kernel is a fast-path kernel");
-    static bool attr_akm = false;
+    static std::atomic<uint64_t> attr_akm{0};
     return launch_one(gemm_kernel_akm<DT, I, TM, TN, CPR>, attr_akm, a, grid, block, lds, s);
   } else {
     if constexpr (DT == 1 && CPR > 0) {
       if (a.dl) {
-        static bool attr_dl = false;
+        static std::atomic<uint64_t> attr_dl{0};
         return launch_one(gemm_kernel_dl<I, TM, TN, CPR>, attr_dl, a, grid, block, lds, s);
       }
     }
-    static bool attr = false;
+    static std::atomic<uint64_t> attr{0};
     return launch_one(gemm_kernel<DT, I, TM, TN, CPR>, attr, a, grid, block, lds, s);
   }
 }

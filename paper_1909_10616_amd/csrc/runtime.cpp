@@ -182,16 +182,15 @@ int compare_on_gpu(const void* C, const void* R, int64_t n, hipStream_t s, doubl
     set_error("device index out of range");
     return GT_EINVAL;
   }
-  unsigned* buf;
-  {
-    std::lock_guard<std::mutex> lk(g_cmp_mu);
-    if (!g_cmp_buf[dev]) {
-      e = hipMalloc(&g_cmp_buf[dev], 2 * sizeof(unsigned));
-      if (e != hipSuccess) return hip_fail(e, "hipMalloc (compare result)");
-    }
-    buf = g_cmp_buf[dev];
+  // The device's 2-word result buffer is held from its clear to the copy
+  // back: comparisons from several threads (any streams) take turns, and
+  // gt_shutdown cannot free the buffer under one in flight.
+  std::lock_guard<std::mutex> lk(g_cmp_mu);
+  if (!g_cmp_buf[dev]) {
+    e = hipMalloc(&g_cmp_buf[dev], 2 * sizeof(unsigned));
+    if (e != hipSuccess) return hip_fail(e, "hipMalloc (compare result)");
   }
-  return compare_into(C, R, n, buf, s, rel);
+  return compare_into(C, R, n, g_cmp_buf[dev], s, rel);
 }
 
 int measure(const gt_config& c, const void* A, const void* B, void* C, int64_t M, int64_t N,
