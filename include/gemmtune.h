@@ -21,8 +21,11 @@
  *   - gemm_run, gt_measure, gt_reference_gemm, gt_compare and the searches may
  *     be called from several host threads at once: each works on the caller's
  *     buffers and stream, and the comparisons take the per-GPU result buffer
- *     in turn. The exception is gt_compare_noalloc, whose calls on one GPU
- *     share one scratch array and must not overlap.
+ *     in turn. Timings (gt_measure, each candidate of a search) take turns
+ *     per GPU, so concurrent searches do not inflate each other's costs
+ *     (other work on the GPU is not held back). The exception is
+ *     gt_compare_noalloc, whose calls on one GPU share one scratch array and
+ *     must not overlap.
  *   - Dimension order is m, k, n everywhere, as in the paper's configuration
  *     (§3.3 Eq.1) and state (§4.1 Eq.5).
  */

@@ -193,11 +193,22 @@ int compare_on_gpu(const void* C, const void* R, int64_t n, hipStream_t s, doubl
   return compare_into(C, R, n, g_cmp_buf[dev], s, rel);
 }
 
+namespace {
+std::mutex g_time_mu[64];    // per device: one timing at a time
+std::mutex g_time_mu_other;  // devices beyond 64, or none current
+}  // namespace
+
 int measure(const gt_config& c, const void* A, const void* B, void* C, int64_t M, int64_t N,
             int64_t K, int dtype, hipStream_t s, int warmup, int runs, double abort_ms,
             double* mean_ms, double* first_ms, int* aborted, RunStats* stats) {
   Lowered lw;
   if (int rc = lower(c, M, N, K, dtype, A, B, C, &lw)) return rc;
+  // Timings on one device take turns (searches in several threads, gt_measure):
+  // each holds the device from its first launch until its last has finished,
+  // so concurrent callers do not inflate each other's costs.
+  int tdev = -1;
+  const bool tdev_ok = hipGetDevice(&tdev) == hipSuccess && tdev >= 0 && tdev < 64;
+  std::lock_guard<std::mutex> timing(tdev_ok ? g_time_mu[tdev] : g_time_mu_other);
   if (warmup < 1) warmup = 1;
   if (runs < 1) runs = 1;
   // events: [0], [1] around the first warm-up launch; [2 + r] before timed

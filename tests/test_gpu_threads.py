@@ -116,3 +116,40 @@ def test_concurrent_compare_returns_each_callers_result(gt):
     assert not errors, errors
     for t in range(n_threads):
         assert got[t] == [expect[t]] * calls, (t, set(got[t]))
+
+
+def test_concurrent_timings_take_turns(gt):
+    """gt_measure from two threads on their own streams, on the 4096³ bf16
+    headline kernel (one workgroup per CU, so two launches in flight at once
+    would each run about twice as long): timings take turns per GPU, and
+    each thread's median stays at the single-threaded median."""
+    import statistics
+    dev = torch.device("cuda:0")
+    cfg = ((16, 2, 8, 16), (128, 1, 1, 32), (16, 4, 2, 32), 16)
+    g = torch.Generator(device="cpu").manual_seed(3)
+    A = torch.randn(4096, 4096, generator=g).to(torch.bfloat16).to(dev)
+    B = torch.randn(4096, 4096, generator=g).to(torch.bfloat16).to(dev)
+    Cs = [torch.empty(4096, 4096, device=dev) for _ in range(2)]
+    solo = statistics.median(gt.gt_measure(cfg, A, B, Cs[0], warmup=2, runs=10)["mean_ms"]
+                             for _ in range(9))
+    print(f"solo median {solo * 1e3:.1f} us", flush=True)
+    got, errors = [[], []], []
+
+    def worker(t):
+        try:
+            s = torch.cuda.Stream(device=dev)
+            for _ in range(15):
+                got[t].append(gt.gt_measure(cfg, A, B, Cs[t], warmup=2, runs=10, stream=s)["mean_ms"])
+        except Exception as e:   # reported below
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(t,)) for t in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    assert not errors, errors
+    for t in range(2):
+        med = statistics.median(got[t])
+        print(f"thread {t} median {med * 1e3:.1f} us", flush=True)
+        assert med < 1.3 * solo, (t, med, solo)
