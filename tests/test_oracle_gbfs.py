@@ -104,3 +104,30 @@ def test_rejects_illegitimate_start(orc):
     with pytest.raises(ValueError):
         orc.gbfs(sp, ((16, 8, 1, 32), (64, 1, 4, 16), (32, 4, 1, 32), 32), 5, 10, 0,
                  lambda c, rk: 1.0)
+
+
+@pytest.mark.parametrize("search", ["gbfs", "random", "na2c"])
+def test_nan_cost_reads_as_a_failed_candidate(orc, search):
+    """A cost that is not a number is no measurement: each search follows
+    exactly the trajectory it follows when those candidates cost +∞, and
+    logs them as +∞."""
+    sp = orc.Space(128, 64, 256, (3, 2, 3), "f32", False)
+    s0 = sp.paper_s0()
+
+    def cost_with(fail):
+        def f(c, r):
+            h = (r * 2654435761) % 997
+            return fail if h % 4 == 0 else 1.0 + h / 997
+        return f
+
+    def run(fail):
+        if search == "gbfs":
+            return orc.gbfs(sp, s0, 3, 120, 7, cost_with(fail))
+        if search == "random":
+            return orc.random_search(sp, 120, 7, cost_with(fail))
+        return orc.na2c(sp, s0, 120, 7, cost_with(fail))
+
+    a, b = run(float("nan")), run(math.inf)
+    assert a["log_ranks"] == b["log_ranks"] and a["log_costs"] == b["log_costs"]
+    assert a["best"] == b["best"] and a["best_cost"] == b["best_cost"]
+    assert math.inf in a["log_costs"] and not any(math.isnan(v) for v in a["log_costs"])
