@@ -108,6 +108,12 @@ def lib():
     if not os.path.exists(LIB_PATH):
         raise GemmTuneError(f"{LIB_PATH} is missing: build it with "
                             "`python -c 'import __graft_entry__ as g; g.build()'`")
+    # One HIP runtime per process: PyTorch ships its own copy and asks for it
+    # by a name without the soname's version, so with the library loaded first
+    # the loader would map the system runtime and PyTorch's side by side, and
+    # the second would find no GPU. With PyTorch loaded first, the library's
+    # libamdhip64.so.7 resolves to the copy already mapped.
+    import torch  # noqa: F401
     L = ctypes.CDLL(LIB_PATH)
     P, i64, u64, i32 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int
     SP, CF = ctypes.POINTER(gt_space), ctypes.POINTER(gt_config)

@@ -9,6 +9,7 @@ import math
 import os
 import re
 import subprocess
+import sys
 import zlib
 
 import numpy as np
@@ -429,3 +430,17 @@ def test_report_arithmetic_exact(gt):
     assert F(1000, 188392750) < F(1, 100)     # the search explores under 1 % of the space
     # 1 ms at 4096³: 137.438953472 TFLOP/s exactly
     assert gt.report(4096, 4096, 4096, "bf16", 1.0, 1, 1, 1)["tflops"] == 137.438953472
+
+
+def test_one_hip_runtime_whatever_the_import_order():
+    """Loading the library before PyTorch must not map a second HIP runtime
+    (two in one process leave the second without a GPU)."""
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "from paper_1909_10616_amd import gemmtune as gt\n"
+            "gt.lib()\n"
+            "import torch\n"
+            "m = {l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l}\n"
+            "print(len(m), sorted(m))\n") % os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    out = subprocess.run([sys.executable, "-c", code], capture_output=True, text=True, timeout=300)
+    assert out.returncode == 0, out.stderr[-2000:]
+    assert out.stdout.split()[0] == "1", out.stdout
