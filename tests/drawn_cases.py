@@ -13,6 +13,7 @@ configuration the GPU runs has first been checked for in-bounds global, LDS
 and C accesses on the host. Drawing uses the library's space only (rank,
 unrank, legitimacy, lowering); nothing here computes a product.
 """
+import os
 import random
 
 ODD = (1, 3, 5, 7, 9, 15)
@@ -56,4 +57,15 @@ def draw_cases(gt, count=96, seed=0x1909_10616):
                 continue
             cases.append((M, N, K, d, dt, mc, akm, c))
             break
+    return cases
+
+
+def cases_with_env_seeds(gt):
+    """The committed list, plus 100 cases per seed named in GT_DRAWN_SEEDS
+    (e.g. "11-14,21-40") for a wider sweep."""
+    cases = draw_cases(gt)
+    for part in filter(None, os.environ.get("GT_DRAWN_SEEDS", "").split(",")):
+        lo, _, hi = part.partition("-")
+        for seed in range(int(lo), int(hi or lo) + 1):
+            cases += draw_cases(gt, count=100, seed=seed)
     return cases

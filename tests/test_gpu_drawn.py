@@ -13,7 +13,7 @@ import numpy as np
 import pytest
 import torch
 
-from drawn_cases import draw_cases
+from drawn_cases import cases_with_env_seeds
 from workloads import make_inputs, make_perceptron_inputs, raw_bytes
 
 pytestmark = pytest.mark.gpu
@@ -31,7 +31,7 @@ def gt():
 def test_drawn_cases_match_oracle(gt, orc):
     dev = torch.device("cuda:0")
     paths = {"dl": 0, "fast": 0, "generic": 0}
-    for i, (M, N, K, d, dt, mc, akm, cfg) in enumerate(draw_cases(gt)):
+    for i, (M, N, K, d, dt, mc, akm, cfg) in enumerate(cases_with_env_seeds(gt)):
         smallint = i % 2 == 0
         dist = "smallint" if smallint else ("normal" if dt == "bf16" else "uniform")
         code = gt.dtype_code(dt) | (gt.A_KMAJOR if akm else 0)

@@ -757,9 +757,9 @@ def test_model_drawn_cases(gt):
     """Every case of the seeded list the GPU parity test runs (random odd
     shapes, one to four levels, both dtypes and layouts, every path) passes
     the kernel models before any of it reaches a GPU."""
-    from drawn_cases import draw_cases
+    from drawn_cases import cases_with_env_seeds
     n = {"dl": 0, "fast": 0, "generic": 0}
-    for M, N, K, d, dt, mc, akm, cfg in draw_cases(gt):
+    for M, N, K, d, dt, mc, akm, cfg in cases_with_env_seeds(gt):
         for k, v in run_models(gt, [cfg], M, N, K, dt, akm).items():
             n[k] += v
     assert n["dl"] >= 5 and n["fast"] >= 10 and n["generic"] >= 40, n
