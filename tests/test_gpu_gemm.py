@@ -12,7 +12,7 @@ import numpy as np
 import pytest
 import torch
 
-from workloads import make_inputs, raw_bytes
+from workloads import make_inputs, make_large_smallint_inputs, raw_bytes
 
 pytestmark = pytest.mark.gpu
 
@@ -336,3 +336,41 @@ def test_search_rejects_a_bad_reference_buffer(gt):
                 torch.zeros(M, N), torch.zeros(N, M, device=dev).t()):
         with pytest.raises(ValueError):
             gt.tune_gbfs(sp, budget=2, A=A, B=B, C=C, c_ref=bad)
+
+
+def test_operands_beyond_4_gib(gt, orc):
+    """Operands of several GiB, split 256 ways along K (M = N = 256, bf16).
+    At K = 9·2^20 (A and B 4.5 GiB each) byte offsets from each operand's
+    start pass 2^32, which the register-staged and generic kernels address
+    with 64-bit offsets; the direct-load ring, whose per-lane offsets from a
+    stage origin are 32-bit, is not chosen there. At K = 7·2^20 the ring is
+    chosen and its lane offsets reach 3.74 GB, near their 2^32 limit. Inputs
+    in {-1, 0, 1}, so every partial sum, in any order, is an integer of at
+    most K < 2^24 in magnitude and exact in fp32: sampled entries, the last
+    rows and columns among them, equal the oracle exactly."""
+    M = N = 256
+    cases = [(9 << 20, [((1, 2, 4, 32), None, (1, 4, 2, 32), 16, 1, 32, (1, 0)),     # register-staged
+                        ((1, 2, 4, 32), None, (1, 4, 2, 32), 16, 8, 4, (0, 0))]),    # generic
+             (7 << 20, [((1, 2, 4, 32), None, (1, 4, 2, 32), 16, 1, 32, (1, 1))])]   # direct-load
+    dev = torch.device("cuda:0")
+    rng = np.random.default_rng(4)
+    rows = np.concatenate([[0, M - 1, M - 1, 0], rng.integers(0, M, 60)])
+    cols = np.concatenate([[0, N - 1, 0, N - 1], rng.integers(0, N, 60)])
+    for K, cfgs in cases:
+        note(f"K = {K}: drawing 2 x {M * K * 2 / 2 ** 30:.2f} GiB of small-integer inputs")
+        A, B = make_large_smallint_inputs(M, N, K, "bf16", 31, bound=1)
+        Ad, Bd = A.to(dev), B.to(dev)
+        ref = orc.gemm_entries(raw_bytes(A), raw_bytes(B), M, N, K, "bf16", rows, cols)
+        del A, B
+        for m, _, n, mfma, ksub, kblk, path in cfgs:
+            cfg = (m, (K // (ksub * kblk) // 256, 256, ksub, kblk), n, mfma)
+            info = gt.lower(cfg, M, N, K, "bf16")
+            note(f"  {gt.fmt_cfg(cfg)} fast={info['fast']} dl={info['dl']} split={info['grid_y']}")
+            assert (info["fast"], info["dl"]) == path and info["grid_y"] == 256
+            C = torch.full((M, N), float("nan"), device=dev)
+            gt.gemm_run(cfg, Ad, Bd, C)
+            torch.cuda.synchronize()
+            got = C.cpu().numpy().astype(np.float64)[rows, cols]
+            assert np.array_equal(got, ref), cfg
+        del Ad, Bd
+        torch.cuda.empty_cache()

@@ -763,3 +763,41 @@ def test_model_drawn_cases(gt):
         for k, v in run_models(gt, [cfg], M, N, K, dt, akm).items():
             n[k] += v
     assert n["dl"] >= 5 and n["fast"] >= 10 and n["generic"] >= 40, n
+
+
+def _wide(K=256, N=256):
+    return (256, N, K, ((1, 2, 4, 32), (K // 32, 1, 1, 32) if K > 256 else (8, 1, 1, 32),
+                        (N // 256, 4, 2, 32), 16))
+
+
+@pytest.mark.parametrize("case", [
+    # (M, N, K, configuration, direct-load expected, ring offsets would wrap):
+    # a 256x256 tile, 32-deep stages
+    (*_wide(K=7 << 20), 1, 0), (*_wide(K=1 << 23), 0, 0), (*_wide(K=9 << 20), 0, 1),
+    (*_wide(N=15 << 22), 1, 0), (*_wide(N=1 << 26), 0, 0), (*_wide(N=9 << 23), 0, 1),
+], ids=["BMxK-below-2^31", "BMxK-at-2^31", "BMxK-offsets-wrap",
+        "BKxN-below-2^31", "BKxN-at-2^31", "BKxN-offsets-wrap"])
+def test_direct_load_offsets_stay_32_bit(gt, case):
+    """The direct-load kernel keeps each lane's global offset from the stage
+    origin in 32 bits (bytes below 2^32 while BM·K and BK·N stay below 2^31
+    elements). Shapes that large are legitimate (operands of several GiB fit
+    in HBM), so lowering leaves the ring for the register-staged kernel,
+    whose offsets are 64-bit, from that bound on (one row early: at the bound
+    itself the offsets would still fit); beyond it they would wrap."""
+    M, N, K, cfg, dl, wraps = case
+    sp = gt.Space(M, N, K, (4, 4, 4), "bf16", True)
+    assert sp.legit(cfg)
+    info = gt.lower(cfg, M, N, K, "bf16")
+    assert info["fast"] == 1 and info["dl"] == dl, info
+    # the ring's per-lane offsets from the stage origins, over every A and B
+    # slot of a stage (the formulas of the direct-load model above)
+    L = levels(cfg)
+    BM, BN, BK, I = L["BM"], L["BN"], L["BK"], L["I"]
+    CPR, cprb = BK // 8, BN >> 3
+    row, chunk = a_slot_chunk(np.arange(BM * CPR), I, BM, CPR)
+    k = np.arange(BK * cprb) >> (lg(BN) - 3)
+    cs = np.arange(BK * cprb) & (cprb - 1)
+    bx = np.array([bswz(int(x), cprb) for x in k])
+    worst = max(int(((row * K + (chunk << 3)) * 2).max()), int(((k * N + ((cs ^ bx) << 3)) * 2).max()))
+    assert (worst >= 2 ** 32) == bool(wraps), worst
+    assert not (dl and wraps)

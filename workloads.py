@@ -80,6 +80,18 @@ def make_inputs(M: int, N: int, K: int, dtype: str, seed: int, dist: str):
     return A.contiguous(), B.contiguous()
 
 
+def make_large_smallint_inputs(M: int, N: int, K: int, dtype: str, seed: int, bound: int = 4):
+    """Small-integer A (M×K) and B (K×N), integers in [-bound, bound] (the
+    "smallint" values of make_inputs for bound 4), drawn directly as int8 so
+    that operands of several GiB need no wider intermediate (a different
+    random stream from make_inputs)."""
+    gen = torch.Generator().manual_seed(seed)
+    t = torch.bfloat16 if dtype == BF16 else torch.float32
+    A = torch.randint(-bound, bound + 1, (M, K), generator=gen, dtype=torch.int8).to(t)
+    B = torch.randint(-bound, bound + 1, (K, N), generator=gen, dtype=torch.int8).to(t)
+    return A.contiguous(), B.contiguous()
+
+
 # The paper's own protocol (§5): perceptron layers Y = WᵀX of sizes
 # (m, k, n) = 512³, 1024³, 2048³ in fp32, d = (4, 2, 4), neighbours between
 # any two levels (Eq.6), s0 = [[m,1,1,1],[k,1],[n,1,1,1]], ρ = 5, and a budget
