@@ -3,6 +3,7 @@
 // normwise difference reduction.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdint>
 
 #include "aux_kernels.h"
@@ -22,20 +23,25 @@ __device__ __forceinline__ float load_in(const void* p, int64_t i, int dtype) {
   return __builtin_bit_cast(float, bits);
 }
 
-// One thread per output; k ascending, fp32 fused multiply-add. dtype 0/1
+// One thread per output (grid-stride over rows and columns, so any M and N
+// fit the grid's limits); k ascending, fp32 fused multiply-add. dtype 0/1
 // (fp32/bf16), plus 16 when A is K-major (element (m, k) at A[k·M + m]).
 __global__ void reference_kernel(const void* __restrict__ A, const void* __restrict__ B,
                                  float* __restrict__ C, int64_t M, int64_t N, int64_t K,
                                  int dtype) {
-  const int64_t col = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
-  const int64_t row = static_cast<int64_t>(blockIdx.y) * blockDim.y + threadIdx.y;
-  if (row >= M || col >= N) return;
   const int dt = dtype & 15;
   const int64_t sr = (dtype & 16) ? 1 : K, sk = (dtype & 16) ? M : 1;
-  float s = 0.0f;
-  for (int64_t l = 0; l < K; ++l)
-    s = fmaf(load_in(A, row * sr + l * sk, dt), load_in(B, l * N + col, dt), s);
-  C[row * N + col] = s;
+  const int64_t rstep = static_cast<int64_t>(gridDim.y) * blockDim.y;
+  const int64_t cstep = static_cast<int64_t>(gridDim.x) * blockDim.x;
+  for (int64_t row = static_cast<int64_t>(blockIdx.y) * blockDim.y + threadIdx.y; row < M;
+       row += rstep)
+    for (int64_t col = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x; col < N;
+         col += cstep) {
+      float s = 0.0f;
+      for (int64_t l = 0; l < K; ++l)
+        s = fmaf(load_in(A, row * sr + l * sk, dt), load_in(B, l * N + col, dt), s);
+      C[row * N + col] = s;
+    }
 }
 
 // out[0] = max |C − R| bits, out[1] = max |R| bits (non-negative floats order
@@ -76,8 +82,11 @@ hipError_t launch_fill_zero(float* p, int64_t n, hipStream_t s) {
 
 hipError_t launch_reference(const void* A, const void* B, float* C, int64_t M, int64_t N, int64_t K,
                             int dtype, hipStream_t s) {
+  if (M <= 0 || N <= 0) return hipSuccess;  // an empty C: nothing to write
   const dim3 block(64, 4);
-  const dim3 grid(static_cast<unsigned>((N + 63) / 64), static_cast<unsigned>((M + 3) / 4));
+  // grid.y is limited to 65535 blocks; the kernel strides over what is left
+  const dim3 grid(static_cast<unsigned>(std::min<int64_t>((N + 63) / 64, int64_t{1} << 20)),
+                  static_cast<unsigned>(std::min<int64_t>((M + 3) / 4, 65535)));
   hipLaunchKernelGGL(reference_kernel, grid, block, 0, s, A, B, C, M, N, K, dtype);
   return hipGetLastError();
 }

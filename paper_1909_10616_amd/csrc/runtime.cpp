@@ -337,10 +337,6 @@ int gt_reference_gemm(const void* A, const void* B, void* C, int64_t M, int64_t 
     gt::set_error("gt_reference_gemm: bad argument");
     return GT_EINVAL;
   }
-  if ((N + 63) / 64 > 2147483647 || (M + 3) / 4 > 65535) {
-    gt::set_error("gt_reference_gemm: shape exceeds the launch grid");
-    return GT_EINVAL;
-  }
   hipError_t e = gt::launch_reference(A, B, static_cast<float*>(C), M, N, K, dtype,
                                       static_cast<hipStream_t>(stream));
   if (e != hipSuccess) {

@@ -374,3 +374,23 @@ def test_operands_beyond_4_gib(gt, orc):
             assert np.array_equal(got, ref), cfg
         del Ad, Bd
         torch.cuda.empty_cache()
+
+
+def test_reference_product_of_a_tall_shape(gt, orc):
+    """The check product the searches compare candidates with, on a shape
+    with more rows than one grid dimension holds blocks of four (393,216 rows
+    > 4·65,535): the kernel strides over the rest. Small integers: sampled
+    entries, the last row among them, equal the oracle exactly."""
+    M, N, K = 3 << 17, 64, 64
+    A, B = make_inputs(M, N, K, "bf16", 41, "smallint")
+    dev = torch.device("cuda:0")
+    R = torch.full((M, N), float("nan"), device=dev)
+    gt.gt_reference_gemm(A.to(dev), B.to(dev), R)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(5)
+    rows = np.concatenate([[M - 1, M - 1, 4 * 65535, 0], rng.integers(0, M, 124)])
+    cols = np.concatenate([[0, N - 1, 7, 0], rng.integers(0, N, 124)])
+    ref = orc.gemm_entries(raw_bytes(A), raw_bytes(B), M, N, K, "bf16", rows, cols)
+    got = R.cpu().numpy().astype(np.float64)
+    assert np.array_equal(got[rows, cols], ref)
+    assert not np.isnan(got).any()
