@@ -15,7 +15,7 @@
  *     that GPU and kept until gt_shutdown(), and (b) the M·N fp32 reference
  *     product of a search whose caller passes no c_ref (freed before the
  *     search returns). Kernel attributes (the dynamic LDS limit) are set once
- *     per kernel and hold no memory.
+ *     per kernel and GPU and hold no memory.
  *   - Space functions (gt_space_size … neighbours) are pure host code, need no
  *     GPU and are thread-safe.
  *   - gemm_run, gt_measure, gt_reference_gemm, gt_compare and the searches may
@@ -147,8 +147,9 @@ int gt_measure(const gt_config* cfg, const void* A, const void* B, void* C,
                int warmup, int runs, double abort_ms, double* mean_ms,
                double* first_ms, int* aborted);
 
-/* Plain (non-MFMA, one thread per output) GPU product in fp32, used by the
- * search as the reference its candidates are checked against. Asynchronous. */
+/* Plain (non-MFMA, one thread per output, any M and N) GPU product in fp32,
+ * used by the search as the reference its candidates are checked against.
+ * Asynchronous. */
 int gt_reference_gemm(const void* A, const void* B, void* C, int64_t M,
                       int64_t N, int64_t K, int dtype, void* stream);
 
