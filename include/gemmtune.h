@@ -133,7 +133,11 @@ int neighbours(const gt_space* sp, const gt_config* s, gt_config* out, int cap,
  * K split (the second K level above 1) two kernels go on the stream: one
  * clears C, then every slice adds its partial product with fp32 atomics, so
  * the order of those adds, and the last bits of C, can differ from launch to
- * launch (results on exactly representable inputs do not). */
+ * launch (results on exactly representable inputs do not). Those are the
+ * GPU's own float atomics, which act on ordinary device memory
+ * (hipMalloc, torch CUDA tensors): C must not be fine-grained or
+ * host-mapped memory (hipMallocManaged, hipHostMalloc) for such
+ * configurations. */
 int gemm_run(const gt_config* cfg, const void* A, const void* B, void* C,
              int64_t M, int64_t N, int64_t K, int dtype, void* stream);
 
