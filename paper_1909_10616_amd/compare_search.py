@@ -1,9 +1,9 @@
-"""G-BFS against equal-budget random search, several seeds, one GPU (§5).
+"""G-BFS against equal-budget random search and N-A2C, several seeds, one GPU (§5).
 
   python -m paper_1909_10616_amd.compare_search --workload gemm4096_bf16 --seeds 10
-      [--budget N] [--t-max S] [--s0 hand|paper] [--methods gbfs,random] [--out FILE.json]
+      [--budget N] [--t-max S] [--s0 hand|paper] [--methods gbfs,random,na2c] [--out FILE.json]
 
-For every seed both searches run on the same resident inputs and the same
+For every seed the chosen searches run on the same resident inputs and the same
 reference product (computed once); every candidate is timed the same way
 (1 warm-up + 10 event-timed runs, output checked). Reported per seed: the
 best cost found (ms, TFLOP/s), configurations timed, search wall time; then
@@ -34,7 +34,7 @@ def main():
     ap.add_argument("--s0", choices=["hand", "paper"], default="hand")
     ap.add_argument("--rho", type=int, default=5)
     ap.add_argument("--methods", default="gbfs,random",
-                    help="comma-separated subset of gbfs,random (random search has no s0)")
+                    help="comma-separated subset of gbfs,random,na2c (random search has no s0)")
     ap.add_argument("--out", default=None)
     ap.add_argument("--progress", type=float, default=0.0,
                     help="> 0: a progress line on stderr at most this often (s)")
@@ -42,8 +42,8 @@ def main():
                     help="name every candidate on stderr before it is launched")
     args = ap.parse_args()
     methods = [m for m in args.methods.split(",") if m]
-    if not methods or any(m not in ("gbfs", "random") for m in methods):
-        raise SystemExit("--methods: a comma-separated subset of gbfs,random")
+    if not methods or any(m not in ("gbfs", "random", "na2c") for m in methods):
+        raise SystemExit("--methods: a comma-separated subset of gbfs,random,na2c")
 
     import torch
     from paper_1909_10616_amd import gemmtune as gt
@@ -66,7 +66,8 @@ def main():
     runs = []
     for seed in range(args.seeds):
         row = {"seed": seed}
-        for name, fn in (("gbfs", gt.tune_gbfs), ("random", gt.tune_random)):
+        for name, fn in (("gbfs", gt.tune_gbfs), ("random", gt.tune_random),
+                         ("na2c", gt.tune_na2c)):
             if name not in methods:
                 continue
             # every candidate is named on stderr before it is launched
@@ -74,6 +75,8 @@ def main():
                       trace_fd=2 if args.trace else -1, progress_s=args.progress)
             if name == "gbfs":
                 kw.update(s0=s0, rho=args.rho)
+            elif name == "na2c":
+                kw.update(s0=s0)
             print(f"seed {seed} {name}: searching", flush=True)
             r = fn(sp, **kw)
             row[name] = {"best": gt.fmt_cfg(r["best"]), "best_ms": r["best_cost"],
