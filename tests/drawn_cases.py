@@ -69,3 +69,27 @@ def cases_with_env_seeds(gt):
         for seed in range(int(lo), int(hi or lo) + 1):
             cases += draw_cases(gt, count=100, seed=seed)
     return cases
+
+
+def draw_small_spaces(gt, count=6, seed=0x5EA5C4, max_legit=3000):
+    """`count` spaces (M, N, K, d, dtype, mfma_coord, a_kmajor) with odd
+    cofactors, small enough that every legitimate configuration can be
+    checked on the CPU (at most `max_legit` of them) and a search on the GPU
+    stays short, each with a legitimate start state."""
+    rng = random.Random(seed)
+    out = []
+    while len(out) < count:
+        M, N = (rng.choice(ODD) << rng.randint(4, 8) for _ in range(2))
+        K = rng.choice(ODD) << rng.randint(4, 9)
+        if M * N * K > (1 << 24):
+            continue
+        d = tuple(rng.randint(2, 4) for _ in range(3))
+        dt = rng.choice(("f32", "bf16"))
+        mc = dt == "bf16" and rng.random() < 0.5
+        akm = rng.random() < 0.25
+        sp = gt.Space(M, N, K, d, dt, mc, a_kmajor=akm)
+        legit = [c for c, j in sp.enumerate() if j]
+        if not 50 <= len(legit) <= max_legit:
+            continue
+        out.append((M, N, K, d, dt, mc, akm))
+    return out

@@ -801,3 +801,19 @@ def test_direct_load_offsets_stay_32_bit(gt, case):
     worst = max(int(((row * K + (chunk << 3)) * 2).max()), int(((k * N + ((cs ^ bx) << 3)) * 2).max()))
     assert (worst >= 2 ** 32) == bool(wraps), worst
     assert not (dl and wraps)
+
+
+def test_model_every_configuration_of_the_search_spaces(gt):
+    """Every legitimate configuration of the small drawn spaces the GPU
+    search test tunes over (a search may time any of them, whatever the
+    timings), every path, passes the kernel models."""
+    from drawn_cases import draw_small_spaces
+    n = {"dl": 0, "fast": 0, "generic": 0}
+    total = 0
+    for M, N, K, d, dt, mc, akm in draw_small_spaces(gt):
+        sp = gt.Space(M, N, K, d, dt, mc, a_kmajor=akm)
+        legit = [c for c, j in sp.enumerate() if j]
+        for k, v in run_models(gt, legit, M, N, K, dt, akm).items():
+            n[k] += v
+        total += len(legit)
+    assert sum(n.values()) == total and n["generic"] > 0 and n["fast"] > 0, n
