@@ -145,12 +145,12 @@ def test_gpu_na2c_replays_in_oracle(gt, orc, case):
 
 
 def test_gpu_searches_on_drawn_odd_spaces_replay_in_oracle(gt, orc):
-    """G-BFS with GPU timing on six small drawn spaces (odd shapes, two to
-    four levels, both dtypes, K-major A on some, the MFMA coordinate on some;
-    every legitimate configuration of each passes the CPU kernel model):
-    the log is consistent, the oracle's Alg.1 fed the logged costs takes the
-    identical trajectory, and the best configuration's product matches the
-    fp64 oracle."""
+    """G-BFS, random search and N-A2C with GPU timing on six small drawn
+    spaces (odd shapes, two to four levels, both dtypes, K-major A on some,
+    the MFMA coordinate on some; every legitimate configuration of each
+    passes the CPU kernel model): each log is consistent, the oracle's
+    search fed the logged costs takes the identical trajectory, and the best
+    configuration's product matches the fp64 oracle."""
     from drawn_cases import draw_small_spaces
     from workloads import make_perceptron_inputs
     dev = torch.device("cuda:0")
@@ -168,24 +168,36 @@ def test_gpu_searches_on_drawn_odd_spaces_replay_in_oracle(gt, orc):
             ref = orc.gemm(raw_bytes(A), raw_bytes(B), M, N, K, dt)
         Ad, Bd = A.to(dev), B.to(dev)
         C = torch.empty(M, N, device=dev)
-        print(f"tune {M}x{N}x{K} d={d} {dt} mfma={mc} kmajor={akm} from {s0} "
-              f"budget {budget} of {len(legit)} legitimate", flush=True)
-        res = gt.tune_gbfs(sp, budget=budget, s0=s0, rho=5, seed=11, A=Ad, B=Bd, C=C)
-        log = res["log"]
-        assert res["timed"] == len(log) <= budget
-        assert res["timed"] == budget or res["stop_reason"] == "queue-empty"
-        assert all(e["status"] in ("ok", "early-abort") for e in log), \
-            [e for e in log if e["status"] not in ("ok", "early-abort")][:3]
-        costs = [e["cost_ms"] for e in log]
-        i = min(range(len(costs)), key=lambda t: (costs[t], t))
-        assert res["best_rank"] == log[i]["rank"] and res["best_cost"] == costs[i]
         os_ = orc.Space(M, N, K, d, dt, mc)
-        table = {e["rank"]: e["cost_ms"] for e in log}
-        rep = orc.gbfs(os_, s0, 5, budget, 11, lambda c, r: table.get(r, math.inf))
-        assert rep["log_ranks"] == [e["rank"] for e in log] and rep["best"] == res["best"]
-        gt.gemm_run(res["best"], Ad, Bd, C, a_kmajor=akm)
-        torch.cuda.synchronize()
-        err = np.abs(C.cpu().numpy().astype(np.float64) - ref).max() / np.abs(ref).max()
-        assert err <= (1e-5 * K ** 0.5 if dt == "f32" else 2e-3), (res["best"], err)
-        print(f"  best {gt.fmt_cfg(res['best'])} after {res['timed']} timings, err {err:.2e}",
-              flush=True)
+        for kind in ("gbfs", "random", "na2c"):
+            print(f"{kind} {M}x{N}x{K} d={d} {dt} mfma={mc} kmajor={akm} from {s0} "
+                  f"budget {budget} of {len(legit)} legitimate", flush=True)
+            kw = dict(budget=budget, seed=11, A=Ad, B=Bd, C=C)
+            if kind == "gbfs":
+                res = gt.tune_gbfs(sp, s0=s0, rho=5, **kw)
+            elif kind == "random":
+                res = gt.tune_random(sp, **kw)
+            else:
+                res = gt.tune_na2c(sp, s0=s0, **kw)
+            log = res["log"]
+            assert res["timed"] == len(log) <= budget
+            assert all(e["status"] in ("ok", "early-abort") for e in log), \
+                [e for e in log if e["status"] not in ("ok", "early-abort")][:3]
+            costs = [e["cost_ms"] for e in log]
+            i = min(range(len(costs)), key=lambda t: (costs[t], t))
+            assert res["best_rank"] == log[i]["rank"] and res["best_cost"] == costs[i]
+            table = {e["rank"]: e["cost_ms"] for e in log}
+            cost = lambda c, r: table.get(r, math.inf)   # noqa: E731
+            if kind == "gbfs":
+                rep = orc.gbfs(os_, s0, 5, budget, 11, cost)
+            elif kind == "random":
+                rep = orc.random_search(os_, budget, 11, cost)
+            else:
+                rep = orc.na2c(os_, s0, budget, 11, cost)
+            assert rep["log_ranks"] == [e["rank"] for e in log] and rep["best"] == res["best"]
+            gt.gemm_run(res["best"], Ad, Bd, C, a_kmajor=akm)
+            torch.cuda.synchronize()
+            err = np.abs(C.cpu().numpy().astype(np.float64) - ref).max() / np.abs(ref).max()
+            assert err <= (1e-5 * K ** 0.5 if dt == "f32" else 2e-3), (kind, res["best"], err)
+            print(f"  best {gt.fmt_cfg(res['best'])} after {res['timed']} timings, err {err:.2e}",
+                  flush=True)
