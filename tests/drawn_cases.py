@@ -21,9 +21,9 @@ MAX_MACS = 1 << 26          # keeps the fp64 oracle product of every case well u
 MAX_WORKGROUPS = 1 << 16    # keeps each launch short
 
 
-def draw_cases(gt, count=96, seed=0x1909_10616):
-    """`count` cases (M, N, K, d, dtype, mfma_coord, a_kmajor, cfg); the
-    list depends on the seed only."""
+def draw_cases(gt, count=96, seed=0x1909_10616, max_macs=MAX_MACS):
+    """`count` cases (M, N, K, d, dtype, mfma_coord, a_kmajor, cfg) of at
+    most `max_macs` multiply-adds; the list depends on the arguments only."""
     rng = random.Random(seed)
     cases = []
     while len(cases) < count:
@@ -35,7 +35,7 @@ def draw_cases(gt, count=96, seed=0x1909_10616):
         else:
             M, N, K = (rng.choice(ODD) << rng.randint(0, 10) for _ in range(3))
             d = tuple(rng.randint(1, 4) for _ in range(3))
-        if M * N * K > MAX_MACS:
+        if M * N * K > max_macs:
             continue
         dt = rng.choice(("f32", "bf16"))
         mc = dt == "bf16" and rng.random() < 0.7
@@ -62,12 +62,14 @@ def draw_cases(gt, count=96, seed=0x1909_10616):
 
 def cases_with_env_seeds(gt):
     """The committed list, plus 100 cases per seed named in GT_DRAWN_SEEDS
-    (e.g. "11-14,21-40") for a wider sweep."""
+    (e.g. "11-14,21-40") for a wider sweep, of at most GT_DRAWN_MAX_MACS
+    multiply-adds each (default 2^26; e.g. 1073741824 for larger shapes)."""
     cases = draw_cases(gt)
+    bound = int(os.environ.get("GT_DRAWN_MAX_MACS", MAX_MACS))
     for part in filter(None, os.environ.get("GT_DRAWN_SEEDS", "").split(",")):
         lo, _, hi = part.partition("-")
         for seed in range(int(lo), int(hi or lo) + 1):
-            cases += draw_cases(gt, count=100, seed=seed)
+            cases += draw_cases(gt, count=100, seed=seed, max_macs=bound)
     return cases
 
 
