@@ -49,6 +49,10 @@ WORKLOADS = {
         Workload("gemm4096_bf16", 4096, 4096, 4096, BF16, 3, "normal_sqrtk", (4, 4, 4), True, 1000),
         Workload("mlp4096x11008x4096_bf16", 4096, 11008, 4096, BF16, 4, "normal002", (4, 4, 4), True, 1000),
         Workload("skinny64x4096x4096_bf16", 64, 4096, 4096, BF16, 4, "normal002", (4, 4, 4), True, 1000),
+        # one GPU's share of the 4096³ product split eight ways along M (its
+        # level-0 grid factor): the slab each GPU would tune and run alone
+        Workload("slab512x4096x4096_bf16", 512, 4096, 4096, BF16, 3, "normal_sqrtk", (4, 4, 4), True,
+                 1000),
     ]
 }
 
