@@ -53,6 +53,9 @@ WORKLOADS = {
         # level-0 grid factor): the slab each GPU would tune and run alone
         Workload("slab512x4096x4096_bf16", 512, 4096, 4096, BF16, 3, "normal_sqrtk", (4, 4, 4), True,
                  1000),
+        # the same eighth of the product split two ways along M and four along N
+        Workload("slab1024x2048x4096_bf16", 1024, 2048, 4096, BF16, 3, "normal_sqrtk", (4, 4, 4), True,
+                 1000),
     ]
 }
 
