@@ -124,3 +124,19 @@ def test_componentwise_error(bench):
     Cg = C.copy()
     Cg[7, 9] += 1e-3 * absab[7, 9]
     assert abs(bench.componentwise_error(W, A, B, Cg, C) - 1e-3) <= 1e-9
+
+
+@pytest.mark.parametrize("methods,ok", [("gbfs,na2c", True), ("random", True), ("gbfs,bogus", False),
+                                        (",", False)])
+def test_compare_search_methods_are_checked_before_any_gpu_work(methods, ok):
+    """compare_search refuses an unknown search before it touches torch or a
+    GPU; a valid list passes that check and stops later, at the missing GPU
+    or at the unknown workload name (so no search ever starts here)."""
+    import subprocess
+    import sys
+    r = subprocess.run([sys.executable, "-m", "paper_1909_10616_amd.compare_search", "--methods", methods,
+                        "--workload", "no_such_workload"],
+                       capture_output=True, text=True, timeout=300,
+                       cwd=os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    assert r.returncode != 0
+    assert ("--methods:" in r.stderr) == (not ok), r.stderr[-500:]
