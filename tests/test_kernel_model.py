@@ -683,6 +683,10 @@ def run_models(gt, cfgs, M, N, K, dtype="bf16", akm=False):
     for c in cfgs:
         info = gt.lower(c, M, N, K, code)
         L = levels(c)
+        # the launch the library chose is the level mapping's (tile, wavefronts,
+        # MFMA size, MFMA tiles per wavefront)
+        assert (info["BM"], info["BN"], info["BK"], info["waves"], info["I"], info["TM"],
+                info["TN"]) == (L["BM"], L["BN"], L["BK"], L["W"], L["I"], L["TM"], L["TN"]), c
         if info["dl"]:
             check_dl(L, info, M, N, K)
             n["dl"] += 1
