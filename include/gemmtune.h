@@ -137,7 +137,10 @@ int neighbours(const gt_space* sp, const gt_config* s, gt_config* out, int cap,
  * GPU's own float atomics, which act on ordinary device memory
  * (hipMalloc, torch CUDA tensors): C must not be fine-grained or
  * host-mapped memory (hipMallocManaged, hipHostMalloc) for such
- * configurations. */
+ * configurations. Errors: GT_EINVAL (null pointer, unknown dtype or a space
+ * make_space refuses), GT_EDIMS (products differ from M, K, N), GT_EILLEGIT
+ * (J = 0), GT_ENOKERNEL, GT_EHIP (launch failure); nothing is launched
+ * unless the result is GT_OK or GT_EHIP. */
 int gemm_run(const gt_config* cfg, const void* A, const void* B, void* C,
              int64_t M, int64_t N, int64_t K, int dtype, void* stream);
 
@@ -145,7 +148,9 @@ int gemm_run(const gt_config* cfg, const void* A, const void* B, void* C,
  * of 10 runs): `warmup` launches (the first one timed on its own), then
  * `runs` back-to-back launches between two HIP events; *mean_ms = elapsed /
  * runs. If the first warm-up launch exceeds abort_ms (> 0), timing stops
- * there, *mean_ms = its time and *aborted = 1. Synchronises the stream. */
+ * there, *mean_ms = its time and *aborted = 1. Synchronises the stream.
+ * Timings on one GPU take turns (see the conventions). Errors: those of
+ * gemm_run, plus GT_EINVAL for a null output pointer. */
 int gt_measure(const gt_config* cfg, const void* A, const void* B, void* C,
                int64_t M, int64_t N, int64_t K, int dtype, void* stream,
                int warmup, int runs, double abort_ms, double* mean_ms,
@@ -153,12 +158,16 @@ int gt_measure(const gt_config* cfg, const void* A, const void* B, void* C,
 
 /* Plain (non-MFMA, one thread per output, any M and N) GPU product in fp32,
  * used by the search as the reference its candidates are checked against.
- * Asynchronous. */
+ * Same operands and layouts as gemm_run (dtype may carry GT_A_KMAJOR); C is
+ * caller-owned M·N fp32. Asynchronous. Errors: GT_EINVAL (null pointer,
+ * M, N or K below 1, unknown dtype), GT_EHIP (launch failure). */
 int gt_reference_gemm(const void* A, const void* B, void* C, int64_t M,
                       int64_t N, int64_t K, int dtype, void* stream);
 
 /* Normwise relative difference max|C − R| / max|R| of two fp32 device
- * arrays of n elements, computed on the GPU. Synchronises the stream. */
+ * arrays of n elements, computed on the GPU (0 when both are all zero, +inf
+ * when only R is, NaN when a difference is NaN). Synchronises the stream.
+ * Errors: GT_EINVAL (null pointer, n < 1), GT_EHIP. */
 int gt_compare(const void* C, const void* R, int64_t n, void* stream,
                double* rel);
 
@@ -174,7 +183,9 @@ int gt_compare(const void* C, const void* R, int64_t n, void* stream,
 int gt_compare_noalloc(const void* C, const void* R, int64_t n, void* stream,
                        double* rel);
 
-/* How a configuration lowers (for reports and tests). */
+/* How a configuration lowers (for reports and tests): the kernel path, tile
+ * and launch gemm_run would use for cfg at M×N×K. Errors: those of gemm_run
+ * before its launch (GT_EINVAL, GT_EDIMS, GT_EILLEGIT, GT_ENOKERNEL). */
 typedef struct gt_kernel_info {
   int32_t I, IK;             /* MFMA instruction size and its K */
   int32_t TM, TN;            /* MFMA tiles per wavefront */
