@@ -280,7 +280,13 @@ int gt_tune_opts_init(gt_tune_opts* opts);
  * that fails to launch or mismatches is logged with cost +inf and the search
  * goes on; a device error that outlives the failing call (a kernel fault)
  * ends the search with GT_EHIP, *out holding the search up to that point and
- * gt_last_error() naming the configuration that was being timed. */
+ * gt_last_error() naming the configuration that was being timed. Errors
+ * before anything is timed: GT_EINVAL (null opts or out, budget or rho below
+ * 1, a space make_space refuses, GPU mode without A, B or C, host memory
+ * exhausted), GT_EDIMS (s0 not a member of the space), GT_EILLEGIT (J(s0) =
+ * 0), GT_EHIP (the reference product could not be allocated or computed).
+ * opts, its log buffer and out are caller-owned; the reference product made
+ * when opts->c_ref is NULL is allocated and freed within the call. */
 int tune_gbfs(const gt_space* sp, const gt_tune_opts* opts, gt_cost_fn cost,
               void* ctx, gt_tune_result* out);
 
