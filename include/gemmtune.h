@@ -47,7 +47,8 @@ typedef enum {
   GT_EILLEGIT = -3,    /* configuration is not legitimate (J = 0) */
   GT_EHIP = -4,        /* a HIP runtime call failed */
   GT_ENOKERNEL = -5,   /* no kernel instantiation for this configuration */
-  GT_ETIMEOUT = -6,    /* search stopped by its time limit before s0 ran */
+  GT_ETIMEOUT = -6,    /* reserved, not returned: a search always times s0
+                          before it checks its time limit */
   GT_ESMALL = -7       /* output buffer too small; *n_out holds the count */
 } gt_status;
 
