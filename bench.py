@@ -61,14 +61,24 @@ def kernel_name(w, info):
     return f"gt::gemm_kernel<{dt}, {info['I']}, {info['TM']}, {info['TN']}, {cpr}>"
 
 
+def _code_only(text: str) -> str:
+    """C++ source without its comments, trailing blanks and empty lines (no
+    string literal in these sources holds a comment marker)."""
+    import re
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", "", text)
+    return "\n".join(line.rstrip() for line in text.splitlines() if line.strip())
+
+
 def kernel_source_hash():
-    """Fingerprint of the sources that hold the GPU kernels' code (how a
-    configuration lowers is part of the launch signature)."""
+    """Fingerprint of the code of the sources that hold the GPU kernels
+    (comments and layout do not count; how a configuration lowers is part
+    of the launch signature)."""
     import hashlib
     h = hashlib.sha256()
     for f in ("gemm_kernel.hpp", "gemm_inst.hip", "aux_kernels.hip"):
-        with open(os.path.join(ROOT, "paper_1909_10616_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_1909_10616_amd", "csrc", f)) as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

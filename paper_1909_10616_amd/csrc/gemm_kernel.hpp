@@ -658,11 +658,12 @@ __device__ void gemm_fast(const KArgs& a, char* smem) {
 // the BM rows, as [m][4] swizzled by swz(). Each fragment read then covers
 // one aligned 1 KiB block, which the 16-byte LDS reads serve without bank
 // conflicts; the stage-wide layout conflicts 2-way at those depths (with
-// 32×32 MFMA, or 32-deep stages, it does not, and is kept). B stays [k][n] with the chunks of row k XOR-ed by
-// bswz(k), and its MFMA operands are read with the transposing LDS read: inside a
-// 16-lane group, lane l receives element (l & 3) of the 8 bytes addressed by
-// lane 4j + (l >> 2) as its j-th value, so lanes addressing rows k0 + (i >> 2),
-// columns n0 + 4(i & 3) hand lane l four consecutive k of column n0 + l.
+// 32×32 MFMA, or 32-deep stages, it does not, and is kept). B stays [k][n]
+// with the chunks of row k XOR-ed by bswz(k), and its MFMA operands are read
+// with the transposing LDS read: inside a 16-lane group, lane l receives
+// element (l & 3) of the 8 bytes addressed by lane 4j + (l >> 2) as its j-th
+// value, so lanes addressing rows k0 + (i >> 2), columns n0 + 4(i & 3) hand
+// lane l four consecutive k of column n0 + l.
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
 // Direct-load instructions per wavefront and stage the kernel keeps offsets
@@ -679,7 +680,7 @@ constexpr int dl_inst_cap(int64_t acc) { return acc + 96 <= 256 ? 8 : 16; }
 __device__ __forceinline__ int bswz(int k, int cprb) {
   const int j = k & 3;
   return (((j << 2) | (((j ^ (j >> 1)) & 1) << 1)) ^ (((k >> 3) & 1) << 3)) & (cprb - 1);
-}  // direct-load instructions per wavefront per stage
+}
 
 // vmcnt field of s_waitcnt on gfx9: bits [3:0] and [15:14]; lgkmcnt [11:8], expcnt [6:4].
 template <int N>

@@ -140,3 +140,13 @@ def test_compare_search_methods_are_checked_before_any_gpu_work(methods, ok):
                        cwd=os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
     assert r.returncode != 0
     assert ("--methods:" in r.stderr) == (not ok), r.stderr[-500:]
+
+
+def test_kernel_fingerprint_ignores_comments_not_code(bench):
+    """The kernel-source fingerprint reads code only: comments and layout do
+    not change it, a changed token does."""
+    code = "int f(int a) {  // doubles\n  /* the\n     body */\n  return 2 * a;\n}\n\n"
+    assert bench._code_only(code) == bench._code_only(code.replace("doubles", "twice")
+                                                      .replace("the\n", "a\n") + "\n// end\n")
+    assert bench._code_only(code) != bench._code_only(code.replace("2 * a", "3 * a"))
+    assert "//" not in bench._code_only(code) and "/*" not in bench._code_only(code)
