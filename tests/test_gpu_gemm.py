@@ -166,6 +166,9 @@ FULL = [
     ("skinny64x4096x4096_bf16", ((1, 2, 2, 16), (8, 4, 1, 128), (64, 4, 1, 16), 16)),
     ("gemm1024_f32", ((8, 2, 2, 32), (32, 1, 4, 8), (8, 2, 2, 32), 0)),
     ("gemm2048_f32", ((16, 2, 2, 32), (64, 1, 4, 8), (16, 2, 2, 32), 0)),
+    # one GPU's share of 4096³ split eight ways, along M and along M and N
+    ("slab512x4096x4096_bf16", ((8, 1, 2, 32), (64, 1, 4, 16), (32, 4, 1, 32), 32)),
+    ("slab1024x2048x4096_bf16", ((8, 2, 2, 32), (64, 1, 2, 32), (32, 2, 2, 16), 16)),
 ]
 
 
